@@ -1,0 +1,239 @@
+#!/usr/bin/env python3
+"""Benchmark: FlexPrefill sparse prefill of one attention layer on one MI355X.
+
+A step is one pass of the whole hot path over one layer: fp_select (pattern search +
+index selection, Algorithms 2-4) followed by fp_sparse_attn (A(Q, K, V, S)).  The default
+workload is the Llama-3-8B-shaped layer at 128k tokens (32 query heads, 8 KV heads,
+d = 128, gamma = 0.95, tau = 0.1, min budget 8 blocks), on seeded synthetic bf16 inputs
+already resident in HBM.  Reported alongside: effective TFLOP/s against the dense causal
+FLOP count, the MFMA fraction of the attention kernel on the blocks it computes, dense
+attention on the same GPU (this library's kernel with every causal block, and PyTorch
+SDPA), and the oracle timed on host cores over a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama128k")
+    ap.add_argument("--gamma", type=float, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--cpu-sample-heads", type=int, default=2)
+    ap.add_argument("--cpu-sample-rows", type=int, default=24)
+    return ap.parse_args()
+
+
+def time_loop(fn, steps, stream):
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for _ in range(steps):
+        fn()
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    return ev[0].elapsed_time(ev[1]) / steps
+
+
+def cpu_baseline(layer, spec, gamma, n_heads, n_rows):
+    """Oracle on host cores over a bounded sample of the same layer, scaled to ms/layer:
+    selection of `n_heads` whole heads, attention on `n_rows` random query-block rows of
+    each of them; per-head and per-row means are scaled to all heads and rows."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        cores = len(os.sched_getaffinity(0))
+    hq, hkv, d, b = spec.hq, spec.hkv, spec.d, spec.block
+    G = hq // hkv
+    cu = layer.cu_seqlens
+    scale = 1.0 / math.sqrt(d)
+    rng = np.random.default_rng(0)
+    heads = list(range(min(n_heads, hq)))
+    t_sel, t_rows, rows_done = 0.0, 0.0, 0
+    total_rows = 0
+    for s in range(len(cu) - 1):
+        total_rows += -(-(int(cu[s + 1]) - int(cu[s])) // b)
+    for h in heads:
+        s = len(cu) - 2                       # the longest (last) sequence
+        t0, t1 = int(cu[s]), int(cu[s + 1])
+        qs, ks, vs = layer.q[t0:t1, h], layer.k[t0:t1, h // G], layer.v[t0:t1, h // G]
+        t = time.perf_counter()
+        r = oracle.select_head(qs, ks, b, gamma, spec.tau, spec.min_budget, scale)
+        t_sel += time.perf_counter() - t
+        nb = r["mask"].shape[0]
+        rows = rng.choice(nb, size=min(n_rows, nb), replace=False)
+        t = time.perf_counter()
+        oracle.sparse_attention_rows(qs, ks, vs, r["mask"], b, scale, rows)
+        t_rows += time.perf_counter() - t
+        rows_done += len(rows)
+    sel_per_head = t_sel / len(heads)
+    row_mean = t_rows / max(rows_done, 1)
+    est_ms = 1e3 * (hq * len(cu[:-1]) * sel_per_head * (1 if len(cu) == 2 else 1) +
+                    hq * total_rows * row_mean)
+    work_s = t_sel + t_rows
+    return {"value": est_ms, "unit": "ms/layer", "cores": int(cores), "kind": "oracle",
+            "sample": (f"float64 numpy oracle: selection of {len(heads)} whole heads and "
+                       f"attention on {rows_done} random query-block rows of the longest "
+                       f"sequence ({work_s:.1f} s of CPU work), scaled to {hq} heads x "
+                       f"{total_rows} rows")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this build runs on exactly one GPU: the FlexPrefill path "
+                                   "needs no cross-GPU communication and multi-GPU runs are "
+                                   "not part of it; run with --gpus 1"}))
+        sys.exit(2)
+    import torch
+    import synth
+    import paper_2502_20766_amd as fpx
+
+    spec = synth.SPECS[args.workload]
+    gamma = spec.gamma if args.gamma is None else args.gamma
+    log(f"[bench] generating {spec.name} (seqlens {spec.seqlens}, {spec.hq}/{spec.hkv} heads, "
+        f"d {spec.d})")
+    t = time.time()
+    layer = synth.make_layer(spec)
+    log(f"[bench] inputs ready in {time.time() - t:.1f}s")
+    dev = torch.device("cuda:0")
+    q = torch.from_numpy(layer.q).to(torch.bfloat16).to(dev)
+    k = torch.from_numpy(layer.k).to(torch.bfloat16).to(dev)
+    v = torch.from_numpy(layer.v).to(torch.bfloat16).to(dev)
+    cu = layer.cu_seqlens
+    stream = torch.cuda.current_stream()
+    shape = fpx.Shape(cu, spec.hq, spec.hkv, spec.d, spec.block)
+    p = fpx.params(gamma, spec.tau, spec.min_budget)
+    ws_sel = torch.empty(max(fpx.select_workspace_size(shape, p), 1), dtype=torch.uint8,
+                         device=dev)
+    ws_att = torch.empty(max(fpx.attn_workspace_size(shape), 1), dtype=torch.uint8, device=dev)
+    idx = fpx.empty_indices(shape, dev)
+    o = torch.empty_like(q)
+
+    def do_select():
+        fpx.select(q, k, cu, gamma, spec.tau, spec.min_budget, out=idx, workspace=ws_sel)
+
+    def do_attn():
+        fpx.sparse_attn(q, k, v, idx, out=o, workspace=ws_att)
+
+    def step():
+        do_select()
+        do_attn()
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} steps")
+    ms_step = time_loop(step, args.steps, stream)
+    ms_select = time_loop(do_select, args.steps, stream)
+    ms_attn = time_loop(do_attn, args.steps, stream)
+    log(f"[bench] step {ms_step:.3f} ms (select {ms_select:.3f}, attn {ms_attn:.3f})")
+
+    seqlens = np.diff(cu).astype(np.int64)
+    f_dense = float(4 * spec.d * spec.hq * np.sum(seqlens * (seqlens + 1) // 2))
+    tiles = int(idx.kb_cnt.sum().item())
+    nbs = -(-seqlens // spec.block)
+    causal_tiles = int(spec.hq * np.sum(nbs * (nbs + 1) // 2))
+    f_comp = float(4 * spec.block * spec.block * spec.d * tiles)
+    attn_tflops = f_comp / (ms_attn * 1e-3) / 1e12
+    pattern = idx.pattern.cpu().numpy()
+
+    dense = {}
+    if not args.no_dense:
+        idx_d = fpx.select(q, k, cu, 1.0, spec.tau, spec.min_budget)
+        fpx.sparse_attn(q, k, v, idx_d, out=o, workspace=ws_att)
+        ms_dense_lib = time_loop(lambda: fpx.sparse_attn(q, k, v, idx_d, out=o,
+                                                         workspace=ws_att), max(2, args.steps // 3),
+                                 stream)
+        dense["library_all_blocks_ms"] = ms_dense_lib
+        dense["library_all_blocks_tflops"] = 4 * spec.block ** 2 * spec.d * causal_tiles / (
+            ms_dense_lib * 1e-3) / 1e12
+        log(f"[bench] dense (library, all blocks) {ms_dense_lib:.3f} ms")
+        try:
+            import torch.nn.functional as F
+            if len(seqlens) == 1:
+                qt = q.transpose(0, 1).unsqueeze(0).contiguous()
+                kt = k.transpose(0, 1).unsqueeze(0).repeat_interleave(
+                    spec.hq // spec.hkv, dim=1).contiguous()
+                vt = v.transpose(0, 1).unsqueeze(0).repeat_interleave(
+                    spec.hq // spec.hkv, dim=1).contiguous()
+                with torch.nn.attention.sdpa_kernel([torch.nn.attention.SDPBackend.FLASH_ATTENTION]):
+                    F.scaled_dot_product_attention(qt, kt, vt, is_causal=True)
+                    ms_sdpa = time_loop(lambda: F.scaled_dot_product_attention(qt, kt, vt,
+                                                                               is_causal=True),
+                                        max(2, args.steps // 3), stream)
+                dense["torch_sdpa_flash_ms"] = ms_sdpa
+                log(f"[bench] dense (torch SDPA flash) {ms_sdpa:.3f} ms")
+                del qt, kt, vt
+        except Exception as e:  # noqa: BLE001
+            dense["torch_sdpa_error"] = str(e)[:200]
+            log(f"[bench] torch SDPA unavailable: {e}")
+    dense_ms = min([x for kk, x in dense.items() if kk.endswith("_ms")] or [float("nan")])
+
+    result = {
+        "metric": "sparse prefill ms/layer + effective TFLOP/s vs dense at 128k; % of MFMA peak",
+        "value": round(ms_step, 4),
+        "unit": "ms/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded vertical-slash / clustered heads, bf16)",
+        "config": {"workload": spec.name, "seqlens": list(map(int, seqlens)), "q_heads": spec.hq,
+                   "kv_heads": spec.hkv, "head_dim": spec.d, "block": spec.block,
+                   "gamma": gamma, "tau": spec.tau, "min_budget_blocks": spec.min_budget},
+        "select_ms": round(ms_select, 4),
+        "attn_ms": round(ms_attn, 4),
+        "effective_tflops": round(f_dense / (ms_step * 1e-3) / 1e12, 2),
+        "attn_tflops_on_computed_blocks": round(attn_tflops, 2),
+        "mfma_frac_on_computed_blocks": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+        "density": round(tiles / causal_tiles, 5),
+        "heads_query_aware": int(np.sum(pattern == 0)),
+        "heads_vertical_slash": int(np.sum(pattern == 1)),
+        "dense": dense,
+        "speedup_vs_dense": round(dense_ms / ms_step, 3) if dense else None,
+        "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "kernel": "sparse_fa_fwd<128>",
+                     "per_launch_flop": f_comp},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle, bounded sample)")
+        result["cpu_baseline"] = cpu_baseline(layer, spec, gamma, args.cpu_sample_heads,
+                                              args.cpu_sample_rows)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,268 @@
+"""Python binding of libflexprefill (FlexPrefill sparse prefill attention for MI355X).
+
+Argument marshalling only: tensors are passed as raw device pointers to the C ABI in
+include/flexprefill.h, and every step of the method runs in the library's HIP kernels.
+PyTorch supplies device memory (outputs and workspaces are allocated with torch) and the
+current stream.  If the library has not been built, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libflexprefill.so")
+
+FP_OK, FP_ERR_INVALID_ARG, FP_ERR_UNSUPPORTED, FP_ERR_WORKSPACE, FP_ERR_HIP = range(5)
+PATTERN_QUERY_AWARE, PATTERN_VERTICAL_SLASH, PATTERN_DENSE = 0, 1, 2
+MAX_BATCH = 64
+MAX_MIN_BUDGET = 64
+
+
+class FlexPrefillError(RuntimeError):
+    def __init__(self, status: int, what: str, detail: str = ""):
+        self.status = status
+        super().__init__(f"{what}: status {status} {detail}".strip())
+
+
+class FpShape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("cu_seqlens", ctypes.POINTER(ctypes.c_int32)),
+                ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("block", ctypes.c_int32)]
+
+
+class FpParams(ctypes.Structure):
+    _fields_ = [("gamma", ctypes.c_float), ("tau", ctypes.c_float),
+                ("min_budget_blocks", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
+                ("force_pattern", ctypes.c_int32)]
+
+
+class FpIndices(ctypes.Structure):
+    _fields_ = [("kb_idx", ctypes.c_void_p), ("kb_cnt", ctypes.c_void_p),
+                ("pattern", ctypes.c_void_p), ("js", ctypes.c_void_p), ("units", ctypes.c_void_p)]
+
+
+_lib_handle = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libflexprefill.so (raises if it has not been built)."""
+    global _lib_handle
+    if _lib_handle is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2502_20766_amd._build`")
+        h = ctypes.CDLL(LIB_PATH)
+        S, P, X = ctypes.POINTER(FpShape), ctypes.POINTER(FpParams), ctypes.POINTER(FpIndices)
+        sz = ctypes.POINTER(ctypes.c_size_t)
+        vp = ctypes.c_void_p
+        h.fp_indices_size.argtypes = [S, sz, sz]
+        h.fp_select_workspace_size.argtypes = [S, P, sz]
+        h.fp_attn_workspace_size.argtypes = [S, sz]
+        h.fp_validate.argtypes = [S, P, ctypes.c_size_t]
+        h.fp_select.argtypes = [S, vp, vp, P, X, vp, ctypes.c_size_t, vp]
+        h.fp_sparse_attn.argtypes = [S, vp, vp, vp, X, ctypes.c_float, vp, vp, ctypes.c_size_t, vp]
+        h.fp_status_string.argtypes = [ctypes.c_int]
+        h.fp_status_string.restype = ctypes.c_char_p
+        h.fp_last_error.argtypes = []
+        h.fp_last_error.restype = ctypes.c_char_p
+        for name in ("fp_indices_size", "fp_select_workspace_size", "fp_attn_workspace_size",
+                     "fp_validate", "fp_select", "fp_sparse_attn"):
+            getattr(h, name).restype = ctypes.c_int
+        _lib_handle = h
+    return _lib_handle
+
+
+def _check(status: int, what: str):
+    if status != FP_OK:
+        h = lib()
+        detail = h.fp_status_string(status).decode()
+        if status == FP_ERR_HIP:
+            detail += " (" + h.fp_last_error().decode() + ")"
+        raise FlexPrefillError(status, what, detail)
+
+
+class Shape:
+    """fp_shape plus the host copy of cu_seqlens it points to."""
+
+    def __init__(self, cu_seqlens, num_q_heads, num_kv_heads, head_dim, block=128):
+        self.cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+        self.c = FpShape(len(self.cu) - 1,
+                         self.cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                         int(num_q_heads), int(num_kv_heads), int(head_dim), int(block))
+        self.block = int(block)
+
+    @property
+    def seqlens(self):
+        return np.diff(self.cu)
+
+    def nb(self):
+        return -(-self.seqlens // self.block)
+
+
+def params(gamma, tau, min_budget=8, softmax_scale=0.0, force_pattern=-1) -> FpParams:
+    return FpParams(float(gamma), float(tau), int(min_budget), float(softmax_scale),
+                    int(force_pattern))
+
+
+def indices_size(shape: Shape):
+    a, b = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib().fp_indices_size(ctypes.byref(shape.c), ctypes.byref(a), ctypes.byref(b)),
+           "fp_indices_size")
+    return a.value, b.value
+
+
+def select_workspace_size(shape: Shape, p: FpParams) -> int:
+    out = ctypes.c_size_t()
+    _check(lib().fp_select_workspace_size(ctypes.byref(shape.c), ctypes.byref(p),
+                                          ctypes.byref(out)), "fp_select_workspace_size")
+    return out.value
+
+
+def attn_workspace_size(shape: Shape) -> int:
+    out = ctypes.c_size_t()
+    _check(lib().fp_attn_workspace_size(ctypes.byref(shape.c), ctypes.byref(out)),
+           "fp_attn_workspace_size")
+    return out.value
+
+
+def validate(shape: Shape, p: FpParams | None, ws_bytes: int) -> int:
+    return lib().fp_validate(ctypes.byref(shape.c), ctypes.byref(p) if p is not None else None,
+                             int(ws_bytes))
+
+
+@dataclass
+class Indices:
+    """Device outputs of select(): torch tensors on the GPU."""
+    shape: Shape
+    kb_idx: object      # int32 [Hq * TRI]
+    kb_cnt: object      # int32 [Hq * NB]
+    pattern: object     # uint8 [B * Hq]
+    js: object          # float32 [B * Hq]
+    units: object       # int32 [B * Hq * 2]
+
+    def c(self) -> FpIndices:
+        return FpIndices(self.kb_idx.data_ptr(), self.kb_cnt.data_ptr(), self.pattern.data_ptr(),
+                         self.js.data_ptr(), self.units.data_ptr())
+
+
+def _stream_ptr(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check_tensor(x, name, ndim):
+    import torch
+    if not (x.is_cuda and x.dtype == torch.bfloat16 and x.dim() == ndim and x.is_contiguous()):
+        raise ValueError(f"{name} must be a contiguous bf16 CUDA tensor of {ndim} dims")
+
+
+def empty_indices(shape: Shape, device):
+    import torch
+    n_idx, n_cnt = indices_size(shape)
+    b, hq = shape.c.batch, shape.c.num_q_heads
+    return Indices(shape,
+                   torch.empty(max(n_idx, 1), dtype=torch.int32, device=device),
+                   torch.empty(max(n_cnt, 1), dtype=torch.int32, device=device),
+                   torch.empty(b * hq, dtype=torch.uint8, device=device),
+                   torch.empty(b * hq, dtype=torch.float32, device=device),
+                   torch.empty(b * hq * 2, dtype=torch.int32, device=device))
+
+
+def select(q, k, cu_seqlens, gamma, tau, min_budget=8, block=128, softmax_scale=0.0,
+           force_pattern=-1, out: Indices | None = None, workspace=None, stream=None) -> Indices:
+    """Pattern search + index selection (Algorithms 2-4) for a packed layer.
+
+    q: [T, Hq, d] bf16 CUDA, k: [T, Hkv, d] bf16 CUDA, cu_seqlens: host ints [B+1]."""
+    import torch
+    _check_tensor(q, "q", 3)
+    _check_tensor(k, "k", 3)
+    shape = Shape(cu_seqlens, q.shape[1], k.shape[1], q.shape[2], block)
+    p = params(gamma, tau, min_budget, softmax_scale, force_pattern)
+    ws_bytes = select_workspace_size(shape, p)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
+    if out is None:
+        out = empty_indices(shape, q.device)
+    oc = out.c()
+    _check(lib().fp_select(ctypes.byref(shape.c), ctypes.c_void_p(q.data_ptr()),
+                           ctypes.c_void_p(k.data_ptr()), ctypes.byref(p), ctypes.byref(oc),
+                           ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                           _stream_ptr(stream)), "fp_select")
+    return out
+
+
+def sparse_attn(q, k, v, indices: Indices, softmax_scale=0.0, out=None, workspace=None,
+                stream=None):
+    """O = A(Q, K, V, S) over the key-block lists in `indices`."""
+    import torch
+    for name, x in (("q", q), ("k", k), ("v", v)):
+        _check_tensor(x, name, 3)
+    shape = indices.shape
+    ws_bytes = attn_workspace_size(shape)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
+    if out is None:
+        out = torch.empty_like(q)
+    ic = indices.c()
+    _check(lib().fp_sparse_attn(ctypes.byref(shape.c), ctypes.c_void_p(q.data_ptr()),
+                                ctypes.c_void_p(k.data_ptr()), ctypes.c_void_p(v.data_ptr()),
+                                ctypes.byref(ic), float(softmax_scale),
+                                ctypes.c_void_p(out.data_ptr()),
+                                ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                                _stream_ptr(stream)), "fp_sparse_attn")
+    return out
+
+
+def indices_from_masks(shape: Shape, masks, device):
+    """Pack host block masks {(s, h): bool [nb, nb]} into the kb_idx / kb_cnt layout
+    (ascending key blocks per row).  Host-side data marshalling for callers that bring
+    their own index sets."""
+    import torch
+    n_idx, n_cnt = indices_size(shape)
+    hq = shape.c.num_q_heads
+    nbs = shape.nb()
+    tri = np.concatenate([[0], np.cumsum(nbs * (nbs + 1) // 2)])
+    nb_off = np.concatenate([[0], np.cumsum(nbs)])
+    TRI, NB = int(tri[-1]), int(nb_off[-1])
+    kb_idx = np.zeros(max(n_idx, 1), dtype=np.int32)
+    kb_cnt = np.zeros(max(n_cnt, 1), dtype=np.int32)
+    for (s, h), m in masks.items():
+        nb = int(nbs[s])
+        for I in range(nb):
+            js = np.nonzero(m[I, :I + 1])[0].astype(np.int32)
+            base = h * TRI + int(tri[s]) + I * (I + 1) // 2
+            kb_idx[base:base + js.size] = js
+            kb_cnt[h * NB + int(nb_off[s]) + I] = js.size
+    b = shape.c.batch
+    return Indices(shape, torch.from_numpy(kb_idx).to(device), torch.from_numpy(kb_cnt).to(device),
+                   torch.zeros(b * hq, dtype=torch.uint8, device=device),
+                   torch.zeros(b * hq, dtype=torch.float32, device=device),
+                   torch.zeros(b * hq * 2, dtype=torch.int32, device=device))
+
+
+def masks_from_indices(indices: Indices):
+    """Unpack device kb_idx / kb_cnt into host bool masks {(s, h): [nb, nb]}."""
+    shape = indices.shape
+    hq = shape.c.num_q_heads
+    nbs = shape.nb()
+    tri = np.concatenate([[0], np.cumsum(nbs * (nbs + 1) // 2)])
+    nb_off = np.concatenate([[0], np.cumsum(nbs)])
+    TRI, NB = int(tri[-1]), int(nb_off[-1])
+    kb_idx = indices.kb_idx.cpu().numpy()
+    kb_cnt = indices.kb_cnt.cpu().numpy()
+    out = {}
+    for s in range(len(nbs)):
+        nb = int(nbs[s])
+        for h in range(hq):
+            m = np.zeros((nb, nb), dtype=bool)
+            for I in range(nb):
+                c = int(kb_cnt[h * NB + int(nb_off[s]) + I])
+                base = h * TRI + int(tri[s]) + I * (I + 1) // 2
+                m[I, kb_idx[base:base + c]] = True
+            out[(s, h)] = m
+    return out

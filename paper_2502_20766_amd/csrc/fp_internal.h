@@ -1,0 +1,93 @@
+// Internal declarations shared by the host orchestration and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/flexprefill.h"
+
+namespace fp {
+
+// Keys of one key block processed per step of the representative-score kernels, and
+// key-chunk length owned by one workgroup of those kernels.
+constexpr int kScoreChunk = 1024;
+constexpr int kHistBuckets = 2048;     // radix-select digit: 11 bits
+
+// Per-call table of packed sequences, passed by value to every kernel.
+struct SeqTable {
+  int32_t n_seq;
+  int32_t max_nb;
+  int32_t cu[FP_MAX_BATCH + 1];       // token offsets
+  int32_t nb_off[FP_MAX_BATCH + 1];   // prefix sums of nb_s = ceil(n_s / block)
+  int32_t ch_off[FP_MAX_BATCH + 1];   // prefix sums of ceil(n_s / kScoreChunk)
+  int64_t tri_off[FP_MAX_BATCH + 1];  // prefix sums of nb_s (nb_s + 1) / 2
+};
+
+// Everything a kernel of the selection pipeline needs.
+struct SelectArgs {
+  SeqTable st;
+  const uint16_t *q;       // [T][Hq][d] bf16
+  const uint16_t *k;       // [T][Hkv][d] bf16
+  int32_t hq, hkv, d, block;
+  int32_t total_tokens;    // T
+  int32_t nb_total;        // NB
+  int64_t tri_total;       // TRI
+  float scale;             // softmax scale
+  float gamma, tau;
+  int32_t min_budget;
+  int32_t force_pattern;
+  // workspace
+  float2 *chunk_stats;     // [ch_total][Hq][block] (max, sum) in log2 units
+  float2 *row_stats;       // [n_seq][Hq][block]
+  float *kbar;             // [NB][Hkv][d]
+  float *qbar;             // [NB][Hq][d]
+  float *a_v;              // [Hq][T]
+  float *a_s;              // [Hq][T]
+  float *flat;             // [Hq][TRI]
+  struct SelState *sel;    // [n_seq][Hq][2]
+  uint32_t *hist_cnt;      // [n_seq][Hq][2][kHistBuckets]
+  unsigned long long *hist_mass;  // [n_seq][Hq][2][kHistBuckets]
+  // outputs
+  int32_t *kb_idx;
+  int32_t *kb_cnt;
+  uint8_t *pattern;
+  float *js;
+  int32_t *units;
+};
+
+// State of one cumulative-mass selection problem (one score vector).
+struct SelState {
+  unsigned long long total;       // fixed-point mass of all units
+  unsigned long long thr;         // ceil(gamma * total)
+  unsigned long long mass_above;  // mass of keys above the current digit range
+  uint32_t cnt_above;             // number of keys above the current digit range
+  uint32_t prefix;                // key bits fixed so far
+  uint32_t key;                   // final threshold key
+  uint32_t need_eq;               // units with key == `key` to take (lowest ids first)
+  uint32_t n_eq;                  // units with key == `key`
+  int32_t idcut;                  // last id taken among key == `key`
+  int32_t k;                      // units selected
+  int32_t mode;                   // 0 active, 1 take all, 2 inactive (other pattern)
+  int32_t n;                      // number of units
+  int32_t pad;
+};
+
+struct AttnArgs {
+  SeqTable st;
+  const uint16_t *q, *k, *v;
+  uint16_t *o;
+  const int32_t *kb_idx;
+  const int32_t *kb_cnt;
+  int32_t hq, hkv, d, block;
+  int32_t nb_total;
+  int64_t tri_total;
+  float scale_log2;        // softmax scale * log2(e)
+  int32_t *row_order;      // [NB] workspace: dispatch order of (s, I) rows
+};
+
+// Launchers (each returns the hipError_t of its launch).
+hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t s);
+hipError_t launch_select_pipeline(const SelectArgs &a, hipStream_t s);
+hipError_t launch_dense_lists(const SelectArgs &a, hipStream_t s);
+
+}  // namespace fp

@@ -1,0 +1,337 @@
+// Representative-block attention scores and block pooling for gfx950.
+//
+// For every (sequence, query head) the last b' = min(block, n) queries Q_hat attend
+// causally to all keys (Section 3, "Representative Query Selection"; Algorithm 3 first
+// step).  From A_hat = softmax(Q_hat K^T / sqrt d) two line scores are reduced:
+//   a_v[j] = sum_r A_hat[r, j] / b'            (vertical lines, Algorithm 3)
+//   a_s[o] = sum_r A_hat[r, i_r - o] / b'      (slash lines, offset o = i - j)
+// A_hat is never stored: pass 1 computes each row's max and sum of exp per chunk of
+// 1024 keys, a combine kernel merges the chunks, pass 2 recomputes the scores tile by
+// tile and reduces columns and diagonals in LDS.  Every sum is in a fixed order (no
+// float atomics), so results are bit-reproducible.  Each pass-2 workgroup owns the slash
+// offsets whose last-row key falls in its chunk and recomputes the 128 keys before the
+// chunk so that it sees those diagonals whole.
+//
+// Block pooling (avgpool with window block_size, aligned at token 0 of each sequence) is
+// a separate streaming kernel used for K (all KV heads) and Q (query-aware heads only).
+#include "fp_internal.h"
+
+namespace fp {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kThreads = 256;
+constexpr int KT = 64;             // keys per tile
+constexpr int PT_PITCH = KT + 1;   // odd pitch: diagonal and column reads are conflict free
+
+__device__ __forceinline__ int seq_of_chunk(const SeqTable &st, int c) {
+  int s = 0;
+  while (s + 1 < st.n_seq && st.ch_off[s + 1] <= c) ++s;
+  return s;
+}
+
+__device__ __forceinline__ int seq_of_block(const SeqTable &st, int blk) {
+  int s = 0;
+  while (s + 1 < st.n_seq && st.nb_off[s + 1] <= blk) ++s;
+  return s;
+}
+
+template <int D>
+__device__ __forceinline__ int k_swz(int chunk, int key) {
+  if constexpr (D == 128) return chunk ^ (key & 15);
+  else return chunk ^ ((key >> 1) & 7);
+}
+
+// Stage keys [kt, kt + KT) of KV head g (rows past n are zero) into LDS, swizzled.
+template <int D>
+__device__ __forceinline__ void stage_k_tile(uint16_t *Ks, const uint16_t *kbase,
+                                             int64_t kv_row, int kt, int n, int tid) {
+  constexpr int KCH = D / 8;
+#pragma unroll
+  for (int it = 0; it < KT * KCH / kThreads; ++it) {
+    const int c = it * kThreads + tid;
+    const int key = c / KCH;
+    const int ch = c % KCH;
+    const int j = kt + key;
+    uint4 val = *reinterpret_cast<const uint4 *>(kbase + (int64_t)min(j, n - 1) * kv_row + ch * 8);
+    if (j >= n) val = make_uint4(0, 0, 0, 0);
+    *reinterpret_cast<uint4 *>(Ks + key * D + k_swz<D>(ch, key) * 8) = val;
+  }
+}
+
+// S^T for 64 keys x the wave's 32 query rows: two 32x32 MFMA blocks.
+template <int D>
+__device__ __forceinline__ void tile_scores(const uint16_t *Ks, const bf16x8 *qf, int lr, int lh,
+                                            f32x16 *sacc) {
+#pragma unroll
+  for (int b2 = 0; b2 < 2; ++b2) {
+    sacc[b2] = f32x16{};
+    const int key = b2 * 32 + lr;
+#pragma unroll
+    for (int k = 0; k < D / 16; ++k) {
+      const bf16x8 kf =
+          *reinterpret_cast<const bf16x8 *>(Ks + key * D + k_swz<D>(2 * k + lh, key) * 8);
+      sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], sacc[b2], 0, 0, 0);
+    }
+  }
+}
+
+// Load the Q_hat^T fragments of the wave's query rows (rows past b' are zero).
+template <int D>
+__device__ __forceinline__ void load_qhat(const SelectArgs &a, int tok0, int n, int h, int r,
+                                          int lh, bf16x8 *qf) {
+  const int bp = min(a.block, n);
+  if (r < bp) {
+    const uint16_t *qp = a.q + ((int64_t)(tok0 + n - bp + r) * a.hq + h) * D + 8 * lh;
+#pragma unroll
+    for (int k = 0; k < D / 16; ++k) qf[k] = *reinterpret_cast<const bf16x8 *>(qp + 16 * k);
+  } else {
+#pragma unroll
+    for (int k = 0; k < D / 16; ++k) qf[k] = bf16x8{};
+  }
+}
+
+// ---------------------------------------------------------------- pass 1: row max / sum
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void rep_stats(SelectArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * D];
+  const int c = blockIdx.x;
+  const int h = blockIdx.y;
+  const int s = seq_of_chunk(a.st, c);
+  const int tok0 = a.st.cu[s];
+  const int n = a.st.cu[s + 1] - tok0;
+  const int bp = min(a.block, n);
+  const int c0 = (c - a.st.ch_off[s]) * kScoreChunk;
+  const int c1 = min(c0 + kScoreChunk, n);
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, lr = lane & 31, lh = lane >> 5;
+  const int r = 32 * w + lr;                 // representative row of this lane
+  const int irow = n - bp + r;               // its absolute position i_r
+  const int G = a.hq / a.hkv;
+  const int64_t kv_row = (int64_t)a.hkv * D;
+  const uint16_t *kbase = a.k + (int64_t)tok0 * kv_row + (int64_t)(h / G) * D;
+  const float sl2 = a.scale * 1.4426950408889634f;
+
+  bf16x8 qf[D / 16];
+  load_qhat<D>(a, tok0, n, h, r, lh, qf);
+  float m = -INFINITY, l = 0.f;
+  for (int kt = c0; kt < c1; kt += KT) {
+    __syncthreads();
+    stage_k_tile<D>(Ks, kbase, kv_row, kt, n, tid);
+    __syncthreads();
+    f32x16 sacc[2];
+    tile_scores<D>(Ks, qf, lr, lh, sacc);
+    float mt = -INFINITY;
+#pragma unroll
+    for (int b2 = 0; b2 < 2; ++b2)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int j = kt + b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
+        float x = sacc[b2][v] * sl2;
+        if (j >= c1 || j > irow || r >= bp) x = -INFINITY;
+        sacc[b2][v] = x;
+        mt = fmaxf(mt, x);
+      }
+    const float mn = fmaxf(m, mt);
+    const float mu = (mn == -INFINITY) ? 0.f : mn;
+    float acc = 0.f;
+#pragma unroll
+    for (int b2 = 0; b2 < 2; ++b2)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc += __builtin_amdgcn_exp2f(sacc[b2][v] - mu);
+    l = l * __builtin_amdgcn_exp2f(m - mu) + acc;
+    m = mn;
+  }
+  // merge the two lanes that share the row (l and l^32)
+  auto pm = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+  auto pl = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l), false, false);
+  const float ma = __uint_as_float(pm[0]), mb = __uint_as_float(pm[1]);
+  const float la = __uint_as_float(pl[0]), lb = __uint_as_float(pl[1]);
+  const float mm = fmaxf(ma, mb);
+  const float mu = (mm == -INFINITY) ? 0.f : mm;
+  // fixed order: lower half's partial first
+  const float lt = la * __builtin_amdgcn_exp2f(ma - mu) + lb * __builtin_amdgcn_exp2f(mb - mu);
+  if (lh == 0) a.chunk_stats[((int64_t)c * a.hq + h) * a.block + r] = make_float2(mm, lt);
+}
+
+// Merge the chunk statistics of each representative row, in chunk order.
+__global__ void rep_stats_combine(SelectArgs a) {
+  const int s = blockIdx.x, h = blockIdx.y, r = threadIdx.x;
+  if (r >= a.block) return;
+  float m = -INFINITY, l = 0.f;
+  for (int c = a.st.ch_off[s]; c < a.st.ch_off[s + 1]; ++c) {
+    const float2 p = a.chunk_stats[((int64_t)c * a.hq + h) * a.block + r];
+    const float mn = fmaxf(m, p.x);
+    const float mu = (mn == -INFINITY) ? 0.f : mn;
+    l = l * __builtin_amdgcn_exp2f(m - mu) + p.y * __builtin_amdgcn_exp2f(p.x - mu);
+    m = mn;
+  }
+  a.row_stats[((int64_t)s * a.hq + h) * a.block + r] = make_float2(m, l);
+}
+
+// ---------------------------------------------------------------- pass 2: line sums
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void rep_lines(SelectArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * D];
+  __shared__ float Pt[128 * PT_PITCH];         // A_hat tile / b', [row][key]
+  __shared__ float acc_s[kScoreChunk];         // owned slash offsets
+  __shared__ float red[4][KT];
+  const int c = blockIdx.x;
+  const int h = blockIdx.y;
+  const int s = seq_of_chunk(a.st, c);
+  const int tok0 = a.st.cu[s];
+  const int n = a.st.cu[s + 1] - tok0;
+  const int bp = min(a.block, n);
+  const int c0 = (c - a.st.ch_off[s]) * kScoreChunk;
+  const int c1 = min(c0 + kScoreChunk, n);
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, lr = lane & 31, lh = lane >> 5;
+  const int r = 32 * w + lr;
+  const int irow = n - bp + r;
+  const int G = a.hq / a.hkv;
+  const int64_t kv_row = (int64_t)a.hkv * D;
+  const uint16_t *kbase = a.k + (int64_t)tok0 * kv_row + (int64_t)(h / G) * D;
+  const float sl2 = a.scale * 1.4426950408889634f;
+
+  float rm = 0.f, rinv = 0.f;
+  if (r < bp) {
+    const float2 st = a.row_stats[((int64_t)s * a.hq + h) * a.block + r];
+    rm = st.x;
+    rinv = 1.f / (st.y * (float)bp);
+  }
+  bf16x8 qf[D / 16];
+  load_qhat<D>(a, tok0, n, h, r, lh, qf);
+  for (int i = tid; i < kScoreChunk; i += kThreads) acc_s[i] = 0.f;
+
+  // keys [c0 - 128, c0) are recomputed for the diagonals owned by this chunk
+  const int kstart = max(c0 - 128, 0);
+  for (int kt = kstart; kt < c1; kt += KT) {
+    __syncthreads();
+    stage_k_tile<D>(Ks, kbase, kv_row, kt, n, tid);
+    __syncthreads();
+    f32x16 sacc[2];
+    tile_scores<D>(Ks, qf, lr, lh, sacc);
+#pragma unroll
+    for (int b2 = 0; b2 < 2; ++b2)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int kl = b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
+        const int j = kt + kl;
+        float p = __builtin_amdgcn_exp2f(sacc[b2][v] * sl2 - rm) * rinv;
+        if (j >= n || j > irow || r >= bp) p = 0.f;
+        Pt[r * PT_PITCH + kl] = p;
+      }
+    __syncthreads();
+    // vertical lines: column sums over the 128 rows, for owned keys
+    if (kt >= c0) {
+      const int col = tid & (KT - 1), quarter = tid >> 6;
+      float cs = 0.f;
+      for (int rr = 32 * quarter; rr < 32 * quarter + 32; ++rr) cs += Pt[rr * PT_PITCH + col];
+      red[quarter][col] = cs;
+    }
+    // slash lines: diagonal o with last-row key jl = n - 1 - o meets this tile for
+    // jl in [kt, kt + KT + bp - 1); rows r with key jl - (bp - 1) + r inside the tile
+    const int jl = kt + tid;
+    if (tid < KT + bp - 1 && jl >= c0 && jl < c1) {
+      const int rlo = max(0, bp - 1 - (jl - kt));
+      const int rhi = min(bp, bp - 1 - (jl - kt) + KT);
+      float ds = 0.f;
+      for (int rr = rlo; rr < rhi; ++rr) ds += Pt[rr * PT_PITCH + (jl - (bp - 1) + rr - kt)];
+      acc_s[jl - c0] += ds;
+    }
+    __syncthreads();
+    if (kt >= c0 && tid < KT) {
+      const int j = kt + tid;
+      if (j < c1)
+        a.a_v[(int64_t)h * a.total_tokens + tok0 + j] =
+            ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < c1 - c0; i += kThreads) {
+    const int jl = c0 + i;
+    a.a_s[(int64_t)h * a.total_tokens + tok0 + (n - 1 - jl)] = acc_s[i];
+  }
+}
+
+// ---------------------------------------------------------------- block pooling
+
+// out[(blk) * H + head][d] = mean over the block's tokens of x[token][head][d].
+// Launched with grid (NB, H); heads whose pattern differs from `only_pattern` are
+// skipped when `pattern` is non-null.
+template <int D>
+__global__ __launch_bounds__(kThreads) void pool_blocks(SeqTable st, const uint16_t *x, int H,
+                                                        int block, float *out,
+                                                        const uint8_t *pattern, int hq,
+                                                        int only_pattern) {
+  constexpr int CH = D / 8;              // 16-byte chunks per row
+  constexpr int PH = kThreads / CH;      // token phases
+  __shared__ float part[PH][D];
+  const int blk = blockIdx.x, head = blockIdx.y;
+  const int s = seq_of_block(st, blk);
+  if (pattern && pattern[s * hq + head] != only_pattern) return;
+  const int tok0 = st.cu[s];
+  const int n = st.cu[s + 1] - tok0;
+  const int J = blk - st.nb_off[s];
+  const int t0 = J * block;
+  const int cntk = min(block, n - t0);
+  const int tid = threadIdx.x, ch = tid % CH, ph = tid / CH;
+  float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int t = ph; t < cntk; t += PH) {
+    const uint4 v = *reinterpret_cast<const uint4 *>(x + ((int64_t)(tok0 + t0 + t) * H + head) * D +
+                                                     ch * 8);
+    const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc[2 * i] += __uint_as_float(wv[i] << 16);
+      acc[2 * i + 1] += __uint_as_float(wv[i] & 0xFFFF0000u);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) part[ph][ch * 8 + i] = acc[i];
+  __syncthreads();
+  if (tid < D) {
+    float sum = 0.f;
+    for (int p = 0; p < PH; ++p) sum += part[p][tid];
+    out[((int64_t)blk * H + head) * D + tid] = sum / (float)cntk;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_rep_scores(const SelectArgs &a, hipStream_t stream) {
+  const int ch_total = a.st.ch_off[a.st.n_seq];
+  dim3 grid(ch_total, a.hq);
+  if (a.d == 128) {
+    hipLaunchKernelGGL(rep_stats<128>, grid, dim3(kThreads), 0, stream, a);
+  } else {
+    hipLaunchKernelGGL(rep_stats<64>, grid, dim3(kThreads), 0, stream, a);
+  }
+  hipLaunchKernelGGL(rep_stats_combine, dim3(a.st.n_seq, a.hq), dim3(128), 0, stream, a);
+  if (a.d == 128) {
+    hipLaunchKernelGGL(rep_lines<128>, grid, dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(pool_blocks<128>, dim3(a.nb_total, a.hkv), dim3(kThreads), 0, stream, a.st,
+                       a.k, a.hkv, a.block, a.kbar, (const uint8_t *)nullptr, a.hq, 0);
+  } else {
+    hipLaunchKernelGGL(rep_lines<64>, grid, dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(pool_blocks<64>, dim3(a.nb_total, a.hkv), dim3(kThreads), 0, stream, a.st,
+                       a.k, a.hkv, a.block, a.kbar, (const uint8_t *)nullptr, a.hq, 0);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_pool_q_query_aware(const SelectArgs &a, hipStream_t stream) {
+  if (a.d == 128)
+    hipLaunchKernelGGL(pool_blocks<128>, dim3(a.nb_total, a.hq), dim3(kThreads), 0, stream, a.st,
+                       a.q, a.hq, a.block, a.qbar, (const uint8_t *)a.pattern, a.hq,
+                       FP_PATTERN_QUERY_AWARE);
+  else
+    hipLaunchKernelGGL(pool_blocks<64>, dim3(a.nb_total, a.hq), dim3(kThreads), 0, stream, a.st,
+                       a.q, a.hq, a.block, a.qbar, (const uint8_t *)a.pattern, a.hq,
+                       FP_PATTERN_QUERY_AWARE);
+  return hipGetLastError();
+}
+
+}  // namespace fp

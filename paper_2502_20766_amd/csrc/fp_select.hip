@@ -1,0 +1,438 @@
+// Cumulative-attention index selection and conversion to key-block lists, for gfx950.
+//
+// Selection (Algorithms 3 and 4, "minimum computational budget"): for a score vector a,
+// order the units by (score desc, id asc) and keep the shortest prefix whose normalised
+// mass reaches gamma -- the greedy optimum of the objective equation (Appendix B).  The
+// set is found without sorting: a three-digit radix select over the fp32 bit patterns
+// (monotone for non-negative floats) finds the threshold key t* such that
+//     mass(keys > t*) < gamma * total <= mass(keys >= t*),
+// then takes the c lowest-id units with key == t* that are still needed.  Masses are
+// accumulated as 2^-48 fixed-point integers, so every sum is exact and independent of
+// atomic order: the selected set is bit-reproducible.  Normalisation by the explicit
+// total is folded into the threshold (prefix >= gamma * total).
+//
+// Conversion: vertical-slash heads extend selected lines to the whole matrix (Section 3,
+// vertical-slash head) at key-block granularity.  A vertical line j marks key block
+// floor(j/b) for every query block at or below it; a slash line o = Delta*b + t marks the
+// block diagonal Delta in every query block whose rows reach an offset-t key in it
+// (t < rows of the query block), and the diagonal Delta+1 when t > 0.  Query-aware heads
+// mark their selected (I, J) units.  Every row then keeps key blocks 0 and I and is
+// topped up to min(m, I+1) blocks (query-aware: highest pooled score first, then lowest
+// J; vertical-slash: nearest the diagonal first) -- the guards of Section 4.1.
+#include "fp_internal.h"
+
+namespace fp {
+
+hipError_t launch_rep_scores(const SelectArgs &a, hipStream_t stream);
+hipError_t launch_pattern_search(const SelectArgs &a, hipStream_t stream);
+hipError_t launch_pool_q_query_aware(const SelectArgs &a, hipStream_t stream);
+hipError_t launch_qa_estimate(const SelectArgs &a, hipStream_t stream);
+
+namespace {
+
+constexpr int kMaxNb = 8192;
+constexpr int kSlice = 4096;          // units per histogram workgroup
+constexpr double kFxScale = 281474976710656.0;   // 2^48
+
+__device__ __forceinline__ unsigned long long to_fx(float x) {
+  return x > 0.f ? (unsigned long long)((double)x * kFxScale) : 0ull;
+}
+
+struct Problem {
+  const float *scores;
+  int n;
+  bool active;
+};
+
+__device__ __forceinline__ Problem problem_of(const SelectArgs &a, int p) {
+  const int kind = p & 1;
+  const int sh = p >> 1;
+  const int s = sh / a.hq, h = sh % a.hq;
+  const int pat = a.pattern[s * a.hq + h];
+  const int tok0 = a.st.cu[s];
+  const int n = a.st.cu[s + 1] - tok0;
+  Problem pr{nullptr, 0, false};
+  if (pat == FP_PATTERN_VERTICAL_SLASH) {
+    pr.scores = (kind == 0 ? a.a_v : a.a_s) + (int64_t)h * a.total_tokens + tok0;
+    pr.n = n;
+    pr.active = true;
+  } else if (pat == FP_PATTERN_QUERY_AWARE && kind == 0) {
+    const int nb = a.st.nb_off[s + 1] - a.st.nb_off[s];
+    pr.scores = a.flat + (int64_t)h * a.tri_total + a.st.tri_off[s];
+    pr.n = nb * (nb + 1) / 2;
+    pr.active = true;
+  }
+  return pr;
+}
+
+__device__ __forceinline__ bool is_selected(const SelState &S, float x, int id) {
+  const uint32_t key = __float_as_uint(x);
+  return key > S.key || (key == S.key && id <= S.idcut);
+}
+
+__global__ void sel_init(SelectArgs a) {
+  const int p = blockIdx.x;
+  for (int b = threadIdx.x; b < kHistBuckets; b += blockDim.x) {
+    a.hist_cnt[(int64_t)p * kHistBuckets + b] = 0u;
+    a.hist_mass[(int64_t)p * kHistBuckets + b] = 0ull;
+  }
+  if (threadIdx.x == 0) {
+    const Problem pr = problem_of(a, p);
+    SelState S = {};
+    S.mode = pr.active ? 0 : 2;
+    S.n = pr.n;
+    S.idcut = -1;
+    a.sel[p] = S;
+  }
+}
+
+template <int PASS>
+__global__ __launch_bounds__(256) void sel_hist(SelectArgs a) {
+  __shared__ uint32_t cnt[kHistBuckets];
+  __shared__ unsigned long long mass[kHistBuckets];
+  const int p = blockIdx.y;
+  const SelState S = a.sel[p];
+  if (S.mode != 0) return;
+  const int start = blockIdx.x * kSlice;
+  if (start >= S.n) return;
+  const Problem pr = problem_of(a, p);
+  for (int b = threadIdx.x; b < kHistBuckets; b += blockDim.x) {
+    cnt[b] = 0u;
+    mass[b] = 0ull;
+  }
+  __syncthreads();
+  constexpr int shift = PASS == 0 ? 21 : (PASS == 1 ? 10 : 0);
+  constexpr uint32_t dmask = PASS == 2 ? 1023u : 2047u;
+  const int end = min(start + kSlice, S.n);
+  for (int i = start + threadIdx.x; i < end; i += blockDim.x) {
+    const float x = pr.scores[i];
+    const uint32_t key = __float_as_uint(x);
+    bool match = true;
+    if (PASS == 1) match = (key >> 21) == (S.prefix >> 21);
+    if (PASS == 2) match = (key >> 10) == (S.prefix >> 10);
+    if (match) {
+      const uint32_t dg = (key >> shift) & dmask;
+      atomicAdd(&cnt[dg], 1u);
+      atomicAdd(&mass[dg], to_fx(x));
+    }
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < kHistBuckets; b += blockDim.x) {
+    if (cnt[b]) {
+      atomicAdd(&a.hist_cnt[(int64_t)p * kHistBuckets + b], cnt[b]);
+      atomicAdd(&a.hist_mass[(int64_t)p * kHistBuckets + b], mass[b]);
+    }
+  }
+}
+
+// Find the digit whose bucket carries the cumulative mass across the threshold.  Thread t
+// owns buckets [2048 - 8(t+1), 2048 - 8t), so thread order is descending key order.
+template <int PASS>
+__global__ __launch_bounds__(256) void sel_scan(SelectArgs a) {
+  __shared__ unsigned long long smass[256];
+  __shared__ uint32_t scnt[256];
+  __shared__ unsigned long long s_total;
+  const int p = blockIdx.x, tid = threadIdx.x;
+  SelState S = a.sel[p];
+  if (S.mode != 0) return;
+  unsigned long long *hm = a.hist_mass + (int64_t)p * kHistBuckets;
+  uint32_t *hc = a.hist_cnt + (int64_t)p * kHistBuckets;
+  const int top = kHistBuckets - 8 * tid;   // exclusive upper bucket
+  unsigned long long bm[8];
+  uint32_t bc[8];
+  unsigned long long lm = 0;
+  uint32_t lc = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    bm[i] = hm[top - 1 - i];
+    bc[i] = hc[top - 1 - i];
+    lm += bm[i];
+    lc += bc[i];
+  }
+  // inclusive scan over threads (Hillis-Steele, integers: exact and order-free)
+  smass[tid] = lm;
+  scnt[tid] = lc;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const unsigned long long vm = tid >= off ? smass[tid - off] : 0ull;
+    const uint32_t vc = tid >= off ? scnt[tid - off] : 0u;
+    __syncthreads();
+    smass[tid] += vm;
+    scnt[tid] += vc;
+    __syncthreads();
+  }
+  const unsigned long long excl_m = smass[tid] - lm;
+  const uint32_t excl_c = scnt[tid] - lc;
+  if (tid == 255) s_total = smass[255];
+  __syncthreads();
+  if (PASS == 0) {
+    const unsigned long long total = s_total;
+    S.total = total;
+    if (total == 0ull) {
+      S.mode = 1;
+    } else {
+      double t = ceil((double)a.gamma * (double)total);
+      unsigned long long thr = (unsigned long long)t;
+      if (thr < 1ull) thr = 1ull;
+      if (thr > total) S.mode = 1;    // never reached: take every unit
+      S.thr = thr;
+    }
+    if (S.mode == 1) {
+      S.key = 0u;
+      S.idcut = 0x7FFFFFFF;
+      S.k = S.n;
+    }
+  }
+  __syncthreads();
+  // all threads zero their buckets for the next pass once everyone has read them
+  for (int i = 0; i < 8; ++i) {
+    hm[top - 1 - i] = 0ull;
+    hc[top - 1 - i] = 0u;
+  }
+  if (S.mode == 1) {
+    if (tid == 0) a.sel[p] = S;
+    return;
+  }
+  constexpr int shift = PASS == 0 ? 21 : (PASS == 1 ? 10 : 0);
+  unsigned long long run = S.mass_above + excl_m;
+  uint32_t runc = S.cnt_above + excl_c;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    if (run < S.thr && run + bm[i] >= S.thr) {
+      const uint32_t digit = (uint32_t)(top - 1 - i);
+      S.prefix |= digit << shift;
+      S.mass_above = run;
+      S.cnt_above = runc;
+      if (PASS == 2) {
+        S.key = S.prefix;
+        S.n_eq = bc[i];
+        const unsigned long long f = bm[i] / bc[i];   // equal keys carry equal mass
+        const unsigned long long need = (S.thr - run + f - 1) / f;
+        S.need_eq = (uint32_t)need;
+        S.k = (int32_t)(runc + need);
+        S.idcut = (need >= bc[i]) ? 0x7FFFFFFF : -1;
+      }
+      a.sel[p] = S;
+    }
+    run += bm[i];
+    runc += bc[i];
+  }
+}
+
+// Lowest-id tie break: find the id of the need_eq-th unit (in id order) whose key equals
+// the threshold key.  Only runs when some but not all of those units are taken.
+__global__ __launch_bounds__(1024) void sel_tie(SelectArgs a) {
+  __shared__ uint32_t wcount[16];
+  __shared__ int found;
+  const int p = blockIdx.x;
+  SelState S = a.sel[p];
+  if (S.mode != 0 || S.idcut != -1) return;
+  const Problem pr = problem_of(a, p);
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  uint32_t running = 0;
+  if (tid == 0) found = -1;
+  __syncthreads();
+  for (int base = 0; base < S.n; base += 1024) {
+    const int i = base + tid;
+    const bool f = i < S.n && __float_as_uint(pr.scores[i]) == S.key;
+    const unsigned long long bal = __ballot(f);
+    if (lane == 0) wcount[w] = (uint32_t)__popcll(bal);
+    __syncthreads();
+    uint32_t before = 0, chunk = 0;
+    for (int k = 0; k < 16; ++k) {
+      if (k < w) before += wcount[k];
+      chunk += wcount[k];
+    }
+    const uint32_t rank = running + before + (uint32_t)__popcll(bal & __lanemask_lt());
+    if (f && rank + 1 == S.need_eq) found = i;
+    __syncthreads();
+    if (found >= 0) break;
+    running += chunk;
+    __syncthreads();
+  }
+  if (tid == 0) {
+    S.idcut = found;
+    a.sel[p] = S;
+  }
+}
+
+// ---------------------------------------------------------------- conversion to lists
+
+__global__ __launch_bounds__(1024) void convert_tiles(SelectArgs a) {
+  __shared__ uint8_t colsel[kMaxNb];
+  __shared__ uint8_t d0[kMaxNb];
+  __shared__ uint8_t d0p[kMaxNb];
+  __shared__ uint8_t d1[kMaxNb + 1];
+  __shared__ int added[16][FP_MAX_MIN_BUDGET];
+  const int s = blockIdx.x / a.hq, h = blockIdx.x % a.hq;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int tok0 = a.st.cu[s];
+  const int n = a.st.cu[s + 1] - tok0;
+  const int b = a.block;
+  const int nb = a.st.nb_off[s + 1] - a.st.nb_off[s];
+  const int last_rows = n - (nb - 1) * b;            // rows of the last query block
+  const int pat = a.pattern[s * a.hq + h];
+  const bool vs = pat == FP_PATTERN_VERTICAL_SLASH;
+  const int p0 = (s * a.hq + h) * 2;
+  const SelState S0 = a.sel[p0];
+  const SelState S1 = a.sel[p0 + 1];
+  const float *flat = a.flat + (int64_t)h * a.tri_total + a.st.tri_off[s];
+
+  if (vs) {
+    for (int i = tid; i <= nb; i += blockDim.x) {
+      if (i < nb) { colsel[i] = 0; d0[i] = 0; d0p[i] = 0; }
+      d1[i] = 0;
+    }
+    __syncthreads();
+    const float *av = a.a_v + (int64_t)h * a.total_tokens + tok0;
+    const float *as = a.a_s + (int64_t)h * a.total_tokens + tok0;
+    for (int j = tid; j < n; j += blockDim.x) {
+      if (is_selected(S0, av[j], j)) colsel[j / b] = 1;
+      if (is_selected(S1, as[j], j)) {
+        const int dl = j / b, t = j % b;
+        d0[dl] = 1;
+        if (t < last_rows) d0p[dl] = 1;
+        if (t > 0) d1[dl + 1] = 1;
+      }
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    a.units[(s * a.hq + h) * 2 + 0] = S0.k;
+    a.units[(s * a.hq + h) * 2 + 1] = vs ? S1.k : 0;
+  }
+
+  const int m = a.min_budget;
+  for (int I = w; I < nb; I += 16) {
+    const bool row_full = (I < nb - 1) || (last_rows == b);
+    const int64_t tri_row = (int64_t)I * (I + 1) / 2;
+    auto sel = [&](int J) -> bool {
+      if (J == 0 || J == I) return true;
+      if (vs) {
+        const int dl = I - J;
+        return colsel[J] || (row_full ? d0[dl] : d0p[dl]) || d1[dl];
+      }
+      return is_selected(S0, flat[tri_row + J], (int)(tri_row + J));
+    };
+    int count = 0;
+    for (int J0 = 0; J0 <= I; J0 += 64) {
+      const int J = J0 + lane;
+      count += __popcll(__ballot(J <= I && sel(J)));
+    }
+    const int target = min(m, I + 1);
+    int jmin = I;          // vertical-slash top-up: every unselected J in [jmin, I)
+    int n_added = 0;       // query-aware top-up: added[w][0..n_added)
+    if (count < target) {
+      int need = target - count;
+      if (vs) {
+        for (int top = I - 1; top >= 0 && need > 0; top -= 64) {
+          const int J = top - lane;
+          const bool un = J >= 0 && !sel(J);
+          const unsigned long long bal = __ballot(un);
+          const int c = __popcll(bal);
+          if (c >= need) {
+            const int rank = __popcll(bal & __lanemask_lt());
+            const unsigned long long pick = __ballot(un && rank == need - 1);
+            jmin = top - (__ffsll((long long)pick) - 1);
+            need = 0;
+          } else {
+            need -= c;
+            jmin = top - 63;
+          }
+        }
+      } else {
+        for (; n_added < need; ++n_added) {
+          float best = -1.f;
+          int bj = 0x7FFFFFFF;
+          for (int J0 = 0; J0 <= I; J0 += 64) {
+            const int J = J0 + lane;
+            if (J > I || sel(J)) continue;
+            bool taken = false;
+            for (int q = 0; q < n_added; ++q) taken |= (added[w][q] == J);
+            if (taken) continue;
+            const float x = flat[tri_row + J];
+            if (x > best || (x == best && J < bj)) { best = x; bj = J; }
+          }
+          for (int off = 32; off > 0; off >>= 1) {
+            const float ob = __shfl_xor(best, off);
+            const int oj = __shfl_xor(bj, off);
+            if (ob > best || (ob == best && oj < bj)) { best = ob; bj = oj; }
+          }
+          if (lane == 0) added[w][n_added] = bj;
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        }
+      }
+    }
+    int32_t *out = a.kb_idx + (int64_t)h * a.tri_total + a.st.tri_off[s] + tri_row;
+    int running = 0;
+    for (int J0 = 0; J0 <= I; J0 += 64) {
+      const int J = J0 + lane;
+      bool f = false;
+      if (J <= I) {
+        f = sel(J) || (J >= jmin && J < I);
+        for (int q = 0; q < n_added; ++q) f |= (added[w][q] == J);
+      }
+      const unsigned long long bal = __ballot(f);
+      if (f) out[running + __popcll(bal & __lanemask_lt())] = J;
+      running += __popcll(bal);
+    }
+    if (lane == 0) a.kb_cnt[(int64_t)h * a.nb_total + a.st.nb_off[s] + I] = running;
+  }
+}
+
+// gamma >= 1: every causal key block, no search (full attention).
+__global__ __launch_bounds__(256) void dense_lists(SelectArgs a) {
+  const int h = blockIdx.y;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= a.nb_total) return;
+  int s = 0;
+  while (s + 1 < a.st.n_seq && a.st.nb_off[s + 1] <= row) ++s;
+  const int I = row - a.st.nb_off[s];
+  int32_t *out = a.kb_idx + (int64_t)h * a.tri_total + a.st.tri_off[s] + (int64_t)I * (I + 1) / 2;
+  for (int J = lane; J <= I; J += 64) out[J] = J;
+  if (lane == 0) a.kb_cnt[(int64_t)h * a.nb_total + row] = I + 1;
+  if (I == 0 && lane == 0) {
+    const int nb = a.st.nb_off[s + 1] - a.st.nb_off[s];
+    a.pattern[s * a.hq + h] = FP_PATTERN_DENSE;
+    a.js[s * a.hq + h] = -1.f;
+    a.units[(s * a.hq + h) * 2 + 0] = nb * (nb + 1) / 2;
+    a.units[(s * a.hq + h) * 2 + 1] = 0;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_dense_lists(const SelectArgs &a, hipStream_t stream) {
+  hipLaunchKernelGGL(dense_lists, dim3((a.nb_total + 3) / 4, a.hq), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_select_pipeline(const SelectArgs &a, hipStream_t stream) {
+  hipError_t e;
+  if ((e = launch_rep_scores(a, stream)) != hipSuccess) return e;
+  if ((e = launch_pattern_search(a, stream)) != hipSuccess) return e;
+  if ((e = launch_pool_q_query_aware(a, stream)) != hipSuccess) return e;
+  if ((e = launch_qa_estimate(a, stream)) != hipSuccess) return e;
+  const int problems = a.st.n_seq * a.hq * 2;
+  int max_units = 0;
+  for (int s = 0; s < a.st.n_seq; ++s) {
+    const int n = a.st.cu[s + 1] - a.st.cu[s];
+    const int nb = a.st.nb_off[s + 1] - a.st.nb_off[s];
+    max_units = max(max_units, max(n, nb * (nb + 1) / 2));
+  }
+  const int slices = (max_units + kSlice - 1) / kSlice;
+  hipLaunchKernelGGL(sel_init, dim3(problems), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(sel_hist<0>, dim3(slices, problems), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(sel_scan<0>, dim3(problems), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(sel_hist<1>, dim3(slices, problems), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(sel_scan<1>, dim3(problems), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(sel_hist<2>, dim3(slices, problems), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(sel_scan<2>, dim3(problems), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(sel_tie, dim3(problems), dim3(1024), 0, stream, a);
+  hipLaunchKernelGGL(convert_tiles, dim3(a.st.n_seq * a.hq), dim3(1024), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace fp

@@ -1,0 +1,183 @@
+"""Helpers comparing the device path with the oracle (test infrastructure).
+
+Selections: the oracle's unit order and float64 prefix masses decide which cut points K
+are acceptable for each selection problem.  K must equal the oracle's K unless the
+prefix mass is within BAND of gamma at the cut (the device accumulates masses in a
+different order and precision); the device's K is read from its diagnostics and only
+accepted if it is one of those cuts.  The expected block mask for that cut is then
+rebuilt with the oracle's own functions and must match the device's lists exactly.
+Pattern decisions must match unless |D_JS - tau| <= BAND, in which case the oracle is
+re-run with the device's pattern forced.
+"""
+from __future__ import annotations
+
+import math
+import sys
+import time
+
+import numpy as np
+
+import oracle
+from oracle import flexprefill as ofp
+
+BAND = 1e-4          # cumulative-mass / JS-distance band around gamma / tau
+O_MAX_ABS = 2e-2     # bf16 output tolerance (max abs error)
+O_MEAN_ABS = 2e-3    # bf16 output tolerance (mean abs error)
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_device(layer):
+    import torch
+    q = torch.from_numpy(layer.q).to(torch.bfloat16).cuda()
+    k = torch.from_numpy(layer.k).to(torch.bfloat16).cuda()
+    v = torch.from_numpy(layer.v).to(torch.bfloat16).cuda()
+    return q, k, v
+
+
+def allowed_cuts(sel: ofp.Selection, gamma: float, band: float = BAND):
+    """Cut points k (number of units taken) acceptable under the mass band."""
+    if gamma >= 1.0:
+        return {sel.scores.size}
+    incl = sel.prefix
+    excl = incl - sel.scores[sel.order]
+    ks = {sel.k}
+    n = sel.scores.size
+    ok = np.nonzero((excl < gamma + band) & (incl >= gamma - band))[0]
+    ks.update(int(i) + 1 for i in ok)
+    if incl[-1] < gamma + band:
+        ks.add(n)
+    return ks
+
+
+def expected_mask_for_cuts(q_seq, k_seq, block, gamma, min_budget, scale, pattern, detail, cuts,
+                           n):
+    """Rebuild the oracle's block mask for the given cut points (oracle functions only)."""
+    nb = -(-n // block)
+    if pattern == oracle.PATTERN_QA:
+        sel = detail["qa"]
+        units = detail["unit_ids"][sel.order[:cuts[0]]]
+        mask = oracle.tiles_from_query_aware(units, nb)
+        return oracle.add_forced_and_min_budget(mask, oracle.PATTERN_QA, min_budget,
+                                                detail["a_map"])
+    sv, ss = detail["v"], detail["s"]
+    mask = oracle.tiles_from_vertical_slash(sv.order[:cuts[0]], ss.order[:cuts[1]], n, block)
+    return oracle.add_forced_and_min_budget(mask, oracle.PATTERN_VS, min_budget)
+
+
+def compare_selection(layer, gpu, gamma, tau, min_budget, heads=None, scale=None):
+    """gpu: dict with 'masks' {(s,h): bool[nb,nb]}, 'pattern' [B*Hq], 'js' [B*Hq],
+    'units' [B*Hq*2] (host arrays).  Returns statistics; raises AssertionError on a
+    mismatch that the bands do not explain."""
+    spec = layer.spec
+    hq, hkv, d = layer.q.shape[1], layer.k.shape[1], layer.q.shape[2]
+    G = hq // hkv
+    scale = 1.0 / math.sqrt(d) if not scale else scale
+    cu = layer.cu_seqlens
+    stats = dict(heads=0, pattern_boundary=0, boundary_problems=0, exact_heads=0,
+                 js_max_err=0.0, tiles=0, density=0.0)
+    sel_total = 0
+    tiles_total = 0
+    for s in range(len(cu) - 1):
+        t0, t1 = int(cu[s]), int(cu[s + 1])
+        n = t1 - t0
+        for h in range(hq):
+            if heads is not None and h not in heads:
+                continue
+            qs, ks = layer.q[t0:t1, h], layer.k[t0:t1, h // G]
+            o = oracle.select_head(qs, ks, spec.block, gamma, tau, min_budget, scale, -1, True)
+            gp = int(gpu["pattern"][s * hq + h])
+            gm = gpu["masks"][(s, h)]
+            stats["heads"] += 1
+            if gamma >= 1.0:
+                assert gp == oracle.PATTERN_DENSE, (s, h, gp)
+                np.testing.assert_array_equal(gm, o["mask"], err_msg=f"dense mask s={s} h={h}")
+                continue
+            gjs = float(gpu["js"][s * hq + h])
+            stats["js_max_err"] = max(stats["js_max_err"], abs(gjs - o["js"]))
+            assert abs(gjs - o["js"]) <= 1e-3, (s, h, gjs, o["js"])
+            if abs(o["js"] - tau) <= BAND:
+                stats["pattern_boundary"] += 1
+                if gp != o["pattern"]:
+                    o = oracle.select_head(qs, ks, spec.block, gamma, tau, min_budget, scale, gp,
+                                           True)
+            assert gp == o["pattern"], f"pattern s={s} h={h}: gpu {gp} oracle {o['pattern']} " \
+                                       f"js {o['js']:.6f} tau {tau}"
+            det = o["detail"]
+            gu = gpu["units"][(s * hq + h) * 2:(s * hq + h) * 2 + 2]
+            if gp == oracle.PATTERN_QA:
+                allowed = [allowed_cuts(det["qa"], gamma)]
+                cuts = (int(gu[0]),)
+                oracle_cuts = (det["qa"].k,)
+            else:
+                allowed = [allowed_cuts(det["v"], gamma), allowed_cuts(det["s"], gamma)]
+                cuts = (int(gu[0]), int(gu[1]))
+                oracle_cuts = (det["v"].k, det["s"].k)
+            for c, al in zip(cuts, allowed):
+                assert c in al, f"s={s} h={h}: device K={c} not in allowed {sorted(al)[:8]}"
+            if cuts != oracle_cuts:
+                stats["boundary_problems"] += sum(int(a != b) for a, b in zip(cuts, oracle_cuts))
+                exp = expected_mask_for_cuts(qs, ks, spec.block, gamma, min_budget, scale, gp, det,
+                                             cuts, n)
+            else:
+                exp = o["mask"]
+                stats["exact_heads"] += 1
+            if not np.array_equal(gm, exp):
+                diff = np.argwhere(gm != exp)
+                raise AssertionError(f"block mask s={s} h={h} pattern {gp}: {len(diff)} tiles "
+                                     f"differ, first {diff[:6].tolist()}")
+            sel_total += int(gm.sum())
+            nb = gm.shape[0]
+            tiles_total += nb * (nb + 1) // 2
+    stats["tiles"] = sel_total
+    stats["density"] = sel_total / max(tiles_total, 1)
+    return stats
+
+
+def compare_outputs(layer, o_gpu, masks, heads=None, row_blocks=None, scale=None, rng=None,
+                    rows_per_head=None):
+    """Oracle A(Q, K, V, S) on the given (oracle-side) masks vs the device output.
+    Returns (max_abs, mean_abs)."""
+    hq, hkv, d = layer.q.shape[1], layer.k.shape[1], layer.q.shape[2]
+    G = hq // hkv
+    block = layer.spec.block
+    scale = 1.0 / math.sqrt(d) if not scale else scale
+    cu = layer.cu_seqlens
+    max_abs, sum_abs, cnt = 0.0, 0.0, 0
+    for s in range(len(cu) - 1):
+        t0, t1 = int(cu[s]), int(cu[s + 1])
+        n = t1 - t0
+        nb = -(-n // block)
+        for h in range(hq):
+            if heads is not None and h not in heads:
+                continue
+            rb = row_blocks
+            if rows_per_head is not None:
+                r = rng if rng is not None else np.random.default_rng(s * 1000 + h)
+                pick = {0, nb - 1} | set(r.integers(0, nb, size=max(rows_per_head - 2, 0)).tolist())
+                rb = sorted(pick)
+            ref = oracle.sparse_attention_rows(layer.q[t0:t1, h], layer.k[t0:t1, h // G],
+                                               layer.v[t0:t1, h // G], masks[(s, h)], block,
+                                               scale, rb)
+            for I, rows in ref.items():
+                got = o_gpu[t0 + I * block:t0 + I * block + rows.shape[0], h].astype(np.float64)
+                err = np.abs(got - rows)
+                max_abs = max(max_abs, float(err.max()))
+                sum_abs += float(err.sum())
+                cnt += err.size
+    return max_abs, sum_abs / max(cnt, 1)
+
+
+class Timer:
+    def __init__(self, what):
+        self.what = what
+
+    def __enter__(self):
+        self.t = time.time()
+        return self
+
+    def __exit__(self, *a):
+        log(f"  [{self.what}: {time.time() - self.t:.2f}s]")

@@ -1,0 +1,204 @@
+"""Device path vs oracle on the same seeded inputs (needs an MI355X and the built library).
+
+Every case goes through the C ABI (Python binding = argument marshalling only)."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from parity import (O_MAX_ABS, O_MEAN_ABS, Timer, compare_outputs, compare_selection, log,
+                          to_device)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2502_20766_amd as fpx
+    fpx.lib()          # fails loudly if the library is missing
+    return fpx
+
+
+def _fpx():
+    import paper_2502_20766_amd as fpx
+    return fpx
+
+
+def run_gpu(layer, gamma, tau, min_budget, force_pattern=-1):
+    fpx = _fpx()
+    q, k, v = to_device(layer)
+    idx = fpx.select(q, k, layer.cu_seqlens, gamma, tau, min_budget, force_pattern=force_pattern)
+    o = fpx.sparse_attn(q, k, v, idx)
+    torch.cuda.synchronize()
+    return dict(masks=fpx.masks_from_indices(idx), pattern=idx.pattern.cpu().numpy(),
+                js=idx.js.cpu().numpy(), units=idx.units.cpu().numpy(),
+                o=o.float().cpu().numpy(), idx=idx, q=q, k=k, v=v)
+
+
+def check_lists_structure(idx, layer, min_budget):
+    """Every row ascending, unique, inside [0, I], holds 0 and I, >= min(m, I+1) blocks."""
+    fpx = _fpx()
+    masks = fpx.masks_from_indices(idx)
+    kb_idx = idx.kb_idx.cpu().numpy()
+    kb_cnt = idx.kb_cnt.cpu().numpy()
+    shape = idx.shape
+    nbs = shape.nb()
+    tri = np.concatenate([[0], np.cumsum(nbs * (nbs + 1) // 2)])
+    nb_off = np.concatenate([[0], np.cumsum(nbs)])
+    hq = shape.c.num_q_heads
+    for s, nb in enumerate(nbs):
+        for h in range(hq):
+            for I in range(nb):
+                c = kb_cnt[h * nb_off[-1] + nb_off[s] + I]
+                base = h * tri[-1] + tri[s] + I * (I + 1) // 2
+                row = kb_idx[base:base + c]
+                assert c >= min(max(min_budget, 2 if I > 0 else 1), I + 1)
+                assert np.all(np.diff(row) > 0) and row[0] == 0 and row[-1] == I
+    return masks
+
+
+# ---------------------------------------------------------------- attention on oracle masks
+
+ATTN_CASES = [
+    # (name, seqlens, hq, hkv, d, mask density)
+    ("tiny-dense-d64", (2048,), 2, 2, 64, 1.0),
+    ("ragged-varlen-d128", (300, 129, 1, 1000, 128), 4, 2, 128, 0.4),
+    ("gqa8-d128-n4096", (4096,), 8, 2, 128, 0.3),
+    ("d64-varlen", (257, 640), 4, 4, 64, 0.5),
+]
+
+
+@pytest.mark.parametrize("case", ATTN_CASES, ids=[c[0] for c in ATTN_CASES])
+def test_sparse_attention_on_oracle_masks(case):
+    name, seqlens, hq, hkv, d, dens = case
+    log(f"[attn-oracle-masks] {name}")
+    fpx = _fpx()
+    kinds = tuple("vs" if h % 2 == 0 else "qa" for h in range(hq))
+    spec = synth.LayerSpec(name, seqlens, hq, hkv, d, 128, kinds, 8, 0.9, 0.1, 2, 777)
+    layer = synth.make_layer(spec)
+    rng = np.random.default_rng(99)
+    masks = {}
+    for s, n in enumerate(seqlens):
+        nb = -(-n // 128)
+        for h in range(hq):
+            m = np.tril(rng.random((nb, nb)) < dens)
+            m[np.arange(nb), 0] = True
+            m[np.arange(nb), np.arange(nb)] = True
+            masks[(s, h)] = m
+    q, k, v = to_device(layer)
+    shape = fpx.Shape(layer.cu_seqlens, hq, hkv, d)
+    idx = fpx.indices_from_masks(shape, masks, q.device)
+    o = fpx.sparse_attn(q, k, v, idx)
+    torch.cuda.synchronize()
+    mx, mean = compare_outputs(layer, o.float().cpu().numpy(), masks)
+    log(f"  max_abs {mx:.3e} mean_abs {mean:.3e}")
+    assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
+
+
+def test_sparse_attention_empty_rows_and_out_of_range_blocks():
+    """A row with no listed blocks yields zeros; listed blocks outside [0, I] are skipped."""
+    fpx = _fpx()
+    spec = synth.LayerSpec("edge", (384,), 2, 1, 128, 128, ("vs", "qa"), 4, 0.9, 0.1, 1, 5)
+    layer = synth.make_layer(spec)
+    q, k, v = to_device(layer)
+    shape = fpx.Shape(layer.cu_seqlens, 2, 1, 128)
+    masks = {(0, 0): np.tril(np.ones((3, 3), bool)), (0, 1): np.tril(np.ones((3, 3), bool))}
+    idx = fpx.indices_from_masks(shape, masks, q.device)
+    # head 1, row 1: no blocks; head 0 row 2: first entry replaced by an invalid block 7
+    nb_total = 3
+    idx.kb_cnt[1 * nb_total + 1] = 0
+    tri_total = 6
+    idx.kb_idx[0 * tri_total + 3] = 7       # row I=2 of head 0 starts at 3: [0,1,2] -> [7,1,2]
+    o = fpx.sparse_attn(q, k, v, idx).float().cpu().numpy()
+    assert np.all(o[128:256, 1] == 0.0)
+    m = np.tril(np.ones((3, 3), bool))
+    m[2, 0] = False
+    ref = oracle.sparse_attention_rows(layer.q[:, 0], layer.k[:, 0], layer.v[:, 0], m, 128,
+                                       1 / math.sqrt(128), [2])
+    assert np.abs(o[256:384, 0] - ref[2]).max() <= O_MAX_ABS
+
+
+# ---------------------------------------------------------------- full path vs oracle
+
+SELECT_CASES = [
+    ("tiny", synth.SPECS["tiny"], None),
+    ("mixed-8h-n8192", synth.SPECS["llama32k"].with_seqlens((8192,), "mixed-8h-n8192")
+     .with_params(hq=8, hkv=2, head_kinds=("vs", "qa") * 4), None),
+    ("ragged-varlen", synth.SPECS["qwen_varlen"].with_seqlens((300, 129, 1, 2000, 4096),
+                                                              "ragged-varlen"), None),
+    ("glm-gqa16-n8192", synth.SPECS["glm64k"].with_seqlens((8192,), "glm-gqa16-n8192"), None),
+]
+
+
+@pytest.mark.parametrize("case", SELECT_CASES, ids=[c[0] for c in SELECT_CASES])
+def test_select_and_attention_vs_oracle(case):
+    name, spec, heads = case
+    log(f"[select+attn] {name} seqlens={spec.seqlens} hq={spec.hq} hkv={spec.hkv} "
+        f"gamma={spec.gamma} tau={spec.tau} m={spec.min_budget}")
+    layer = synth.make_layer(spec)
+    g = run_gpu(layer, spec.gamma, spec.tau, spec.min_budget)
+    check_lists_structure(g["idx"], layer, spec.min_budget)
+    with Timer("oracle selection"):
+        st = compare_selection(layer, g, spec.gamma, spec.tau, spec.min_budget)
+    log(f"  {st}")
+    mx, mean = compare_outputs(layer, g["o"], g["masks"], rows_per_head=6)
+    log(f"  output max_abs {mx:.3e} mean_abs {mean:.3e}")
+    assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
+
+
+@pytest.mark.parametrize("force", [0, 1])
+def test_forced_patterns(force):
+    spec = SELECT_CASES[1][1]
+    log(f"[forced pattern {force}] {spec.name}")
+    layer = synth.make_layer(spec)
+    g = run_gpu(layer, spec.gamma, spec.tau, spec.min_budget, force_pattern=force)
+    assert np.all(g["pattern"] == force)
+    # compare against the oracle with the same forced pattern
+    hq = spec.hq
+    ores = oracle.select(layer.q, layer.k, layer.cu_seqlens, spec.block, spec.gamma, spec.tau,
+                         spec.min_budget, force_pattern=force)
+    for h in range(hq):
+        np.testing.assert_array_equal(g["masks"][(0, h)], ores[0][h]["mask"],
+                                      err_msg=f"head {h}")
+
+
+@pytest.mark.parametrize("gamma", [1.0])
+def test_gamma_one_is_dense(gamma):
+    spec = synth.SPECS["tiny"]
+    log(f"[gamma=1 dense] {spec.name}")
+    layer = synth.make_layer(spec)
+    g = run_gpu(layer, gamma, spec.tau, spec.min_budget)
+    assert np.all(g["pattern"] == oracle.PATTERN_DENSE)
+    n = spec.seqlens[0]
+    for h in range(spec.hq):
+        ref = oracle.dense_causal_attention(layer.q[:, h], layer.k[:, h], layer.v[:, h],
+                                            1 / math.sqrt(spec.d))
+        err = np.abs(g["o"][:n, h] - ref)
+        log(f"  head {h} max_abs {err.max():.3e} mean_abs {err.mean():.3e}")
+        assert err.max() <= O_MAX_ABS and err.mean() <= O_MEAN_ABS
+
+
+def test_tau_zero_gives_only_vertical_slash():
+    spec = SELECT_CASES[1][1]
+    layer = synth.make_layer(spec)
+    g = run_gpu(layer, spec.gamma, 0.0, spec.min_budget)
+    assert np.all(g["pattern"] == oracle.PATTERN_VS)
+
+
+def test_determinism_bitwise():
+    spec = SELECT_CASES[1][1]
+    log(f"[determinism] {spec.name}")
+    layer = synth.make_layer(spec)
+    a = run_gpu(layer, spec.gamma, spec.tau, spec.min_budget)
+    b = run_gpu(layer, spec.gamma, spec.tau, spec.min_budget)
+    for key in ("pattern", "js", "units"):
+        np.testing.assert_array_equal(a[key], b[key])
+    np.testing.assert_array_equal(a["idx"].kb_cnt.cpu().numpy(), b["idx"].kb_cnt.cpu().numpy())
+    np.testing.assert_array_equal(a["idx"].kb_idx.cpu().numpy(), b["idx"].kb_idx.cpu().numpy())
+    np.testing.assert_array_equal(a["o"], b["o"])
