@@ -13,7 +13,8 @@
 //     bank-conflict free;
 //   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (Q^T fragments live in registers), so each
 //     lane owns one query row and 64 of the 128 keys: the row max needs one lane swap;
-//   * online softmax in the log2 domain (exp2 with log2(e) folded into the scale);
+//   * online softmax in the log2 domain (exp2 with log2(e) folded into the scale), the
+//     O rescale skipped when no row of the wave sees a new maximum;
 //   * O^T += V^T P^T on the same MFMA: P^T is already in B-operand layout (the key order
 //     inside each 16-key step is permuted identically on both operands), and O^T keeps
 //     one query row per lane, so the rescale by exp2(m_old - m_new) is per lane.
@@ -27,6 +28,8 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int BM = 128;  // queries per workgroup (one query block)
 constexpr int BN = 128;  // keys per tile (one key block)
@@ -43,21 +46,58 @@ __device__ __forceinline__ float wave_pair_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// 16-byte chunk swizzle of the K tile row `key` (D/8 chunks per row)
+// Geometry of one 64-key stage in LDS (K and V both row-major [key][d], bf16).
 template <int D>
-__device__ __forceinline__ int k_swz(int chunk, int key) {
-  if constexpr (D == 128) return chunk ^ (key & 15);
-  else return chunk ^ ((key >> 1) & 7);
+struct Stage {
+  static constexpr int RB = 2 * D;                 // bytes per key row
+  static constexpr int CPR = RB / 16;              // 16-byte chunks per row
+  static constexpr int KEYS = 64;
+  static constexpr int BYTES = KEYS * RB;          // one tile (K or V)
+  static constexpr int RPI = 1024 / RB;            // rows written by one wave-wide DMA
+  static constexpr int DMA_PER_WAVE = BYTES / 1024 / 4;
+};
+
+// 16-byte chunk swizzles (XOR, so the same function maps logical <-> physical).
+// K: the 32 rows read by one half-wave at the same chunk land on distinct banks.
+template <int D>
+__device__ __forceinline__ int swz_k(int y, int r) {
+  if constexpr (D == 128) return y ^ (r & 15);
+  else return y ^ ((r >> 1) & 7);
+}
+// V: the 4 consecutive rows x 4 chunks read by one half-wave transposing load are distinct.
+template <int D>
+__device__ __forceinline__ int swz_v(int y, int r) {
+  if constexpr (D == 128) return y ^ ((r & 3) << 2);
+  else return y ^ (((r >> 1) & 1) << 2);
 }
 
-// 8-byte unit swizzle of the transposed V tile row `d` (32 units of 4 keys per row)
-__device__ __forceinline__ int v_swz(int unit, int d) { return unit ^ (((d >> 2) ^ d) & 31); }
+// Issue the DMA of one 64-key stage (keys k0 .. k0+63 of the sequence; rows past the
+// sequence end re-read its last row, they are masked out by the caller).
+template <int D>
+__device__ __forceinline__ void stage_dma(uint8_t *ks, uint8_t *vs, const uint16_t *kbase,
+                                          const uint16_t *vbase, int64_t kv_row, int k0,
+                                          int kvalid, int w, int lane) {
+  using S = Stage<D>;
+#pragma unroll
+  for (int i = 0; i < S::DMA_PER_WAVE; ++i) {
+    const int q = i * 4 + w;
+    const int r = q * S::RPI + lane / S::CPR;
+    const int phys = lane % S::CPR;
+    const int64_t row = (int64_t)(k0 + min(r, kvalid - 1)) * kv_row;
+    __builtin_amdgcn_global_load_lds(
+        (__attribute__((address_space(1))) void *)(kbase + row + swz_k<D>(phys, r) * 8),
+        (__attribute__((address_space(3))) void *)(ks + q * 1024), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(
+        (__attribute__((address_space(1))) void *)(vbase + row + swz_v<D>(phys, r) * 8),
+        (__attribute__((address_space(3))) void *)(vs + q * 1024), 16, 0, 0);
+  }
+}
 
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void sparse_fa_fwd(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[BN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * BN];
+  using S = Stage<D>;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[4 * S::BYTES];  // [2 stages][K, V]
 
   const int G = a.hq / a.hkv;
   const int bid = blockIdx.x;
@@ -82,6 +122,8 @@ void sparse_fa_fwd(AttnArgs a) {
   const int lane = tid & 63;
   const int lr = lane & 31;
   const int lh = lane >> 5;
+  const int g16 = lane >> 4;
+  const int i16 = lane & 15;
 
   const int cnt = min(a.kb_cnt[(int64_t)h * a.nb_total + a.st.nb_off[s] + I], I + 1);
   const int32_t *list = a.kb_idx + (int64_t)h * a.tri_total + a.st.tri_off[s] +
@@ -91,142 +133,130 @@ void sparse_fa_fwd(AttnArgs a) {
   constexpr int KS = D / 16;
   bf16x8 qf[KS];
   const int qrow = 32 * w + lr;
-  if (q0 + qrow < n) {
-    const uint16_t *qp = a.q + ((int64_t)(tok0 + q0 + qrow) * a.hq + h) * D + 8 * lh;
+  {
+    const int qr = min(q0 + qrow, n - 1);
+    const uint16_t *qp = a.q + ((int64_t)(tok0 + qr) * a.hq + h) * D + 8 * lh;
 #pragma unroll
     for (int k = 0; k < KS; ++k) qf[k] = *reinterpret_cast<const bf16x8 *>(qp + 16 * k);
-  } else {
-#pragma unroll
-    for (int k = 0; k < KS; ++k) qf[k] = bf16x8{};
   }
 
   constexpr int DB = D / 32;
   f32x16 oacc[DB];
 #pragma unroll
   for (int i = 0; i < DB; ++i) oacc[i] = f32x16{};
-  float m_run = -INFINITY;
+  float m_ref = -INFINITY;   // reference max (raw logit units) of this lane's row
   float l_run = 0.f;
+  const float c = a.scale_log2;
 
   const int64_t kv_row = (int64_t)a.hkv * D;  // elements between consecutive tokens
   const uint16_t *kbase = a.k + (int64_t)tok0 * kv_row + (int64_t)g * D;
   const uint16_t *vbase = a.v + (int64_t)tok0 * kv_row + (int64_t)g * D;
 
-  for (int t = 0; t < cnt; ++t) {
-    const int J = list[t];
-    if (J < 0 || J > I) continue;
-    const int k0 = J * BN;
-    const int kvalid = min(BN, n - k0);
+  // stage t covers keys J*128 + 64*(t&1) .. +63 of block J = list[t >> 1]
+  const int n_stages = 2 * cnt;
+  auto stage_k0 = [&](int t) -> int {
+    const int J = list[t >> 1];
+    if (J < 0 || J > I) return -1;
+    const int k0 = J * BN + 64 * (t & 1);
+    return k0 < n ? k0 : -1;
+  };
 
-    __syncthreads();
-    // ---- K tile -> LDS (row-major, swizzled 16-byte chunks)
-    constexpr int KCH = D / 8;
-#pragma unroll
-    for (int it = 0; it < BN * KCH / kThreads; ++it) {
-      const int c = it * kThreads + tid;
-      const int key = c / KCH;
-      const int ch = c % KCH;
-      // rows past the sequence end read the last valid row and are zeroed (no branch)
-      uint4 val = *reinterpret_cast<const uint4 *>(
-          kbase + (int64_t)(k0 + min(key, kvalid - 1)) * kv_row + ch * 8);
-      if (key >= kvalid) val = make_uint4(0, 0, 0, 0);
-      *reinterpret_cast<uint4 *>(Ks + key * D + k_swz<D>(ch, key) * 8) = val;
+  int k0_next = n_stages > 0 ? stage_k0(0) : -1;
+  if (k0_next >= 0)
+    stage_dma<D>(lds, lds + S::BYTES, kbase, vbase, kv_row, k0_next, min(64, n - k0_next), w,
+                 lane);
+  for (int t = 0; t < n_stages; ++t) {
+    const int k0 = k0_next;
+    uint8_t *ks = lds + (t & 1) * 2 * S::BYTES;
+    uint8_t *vs = ks + S::BYTES;
+    __builtin_amdgcn_s_waitcnt(0);      // this wave's DMA of stage t has landed
+    __syncthreads();                    // ... and every wave's; stage t-1 reads are done
+    k0_next = (t + 1 < n_stages) ? stage_k0(t + 1) : -1;
+    if (k0_next >= 0) {
+      uint8_t *kn = lds + ((t + 1) & 1) * 2 * S::BYTES;
+      stage_dma<D>(kn, kn + S::BYTES, kbase, vbase, kv_row, k0_next, min(64, n - k0_next), w,
+                   lane);
     }
-    // ---- V tile -> LDS transposed: each thread moves a 4-key x 4-d block
-    constexpr int DQ = D / 4;
+    if (k0 < 0) continue;
+
+    // ---- S^T = K Q^T for the stage's 64 keys (2 blocks of 32 keys x 32 queries)
+    f32x16 sacc[2];
 #pragma unroll
-    for (int it = 0; it < BN * DQ / 4 / kThreads; ++it) {
-      const int u = it * kThreads + tid;
-      const int dq = u % DQ;
-      const int kq = u / DQ;
-      uint2 r[4];
+    for (int b2 = 0; b2 < 2; ++b2) {
+      sacc[b2] = f32x16{};
+      const int r = b2 * 32 + lr;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int key = 4 * kq + e;
-        r[e] = *reinterpret_cast<const uint2 *>(
-            vbase + (int64_t)(k0 + min(key, kvalid - 1)) * kv_row + 4 * dq);
-        if (key >= kvalid) r[e] = make_uint2(0, 0);
-      }
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const uint32_t sh = (c & 1) ? 16u : 0u;
-        const uint32_t w0 = ((c < 2 ? r[0].x : r[0].y) >> sh) & 0xFFFFu;
-        const uint32_t w1 = ((c < 2 ? r[1].x : r[1].y) >> sh) & 0xFFFFu;
-        const uint32_t w2 = ((c < 2 ? r[2].x : r[2].y) >> sh) & 0xFFFFu;
-        const uint32_t w3 = ((c < 2 ? r[3].x : r[3].y) >> sh) & 0xFFFFu;
-        const int d = 4 * dq + c;
-        *reinterpret_cast<uint2 *>(Vt + d * BN + v_swz(kq, d) * 4) =
-            make_uint2(w0 | (w1 << 16), w2 | (w3 << 16));
+      for (int k = 0; k < KS; ++k) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(
+            ks + r * S::RB + swz_k<D>(2 * k + lh, r) * 16);
+        sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], sacc[b2], 0, 0, 0);
       }
     }
-    __syncthreads();
-
-    // ---- two halves of 64 keys: S^T = K Q^T, online softmax, O^T += V^T P^T
-    const bool diag = (J == I);
+    // ---- causal mask (diagonal block only) and row max in raw logit units
+    const int kq = k0 - q0;             // key offset relative to the query block start
+    if (kq >= 0) {
+      // diagonal block: keys after this lane's query row get -inf
 #pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      f32x16 sacc[2];
-#pragma unroll
-      for (int b2 = 0; b2 < 2; ++b2) {
-        sacc[b2] = f32x16{};
-        const int key = (2 * hf + b2) * 32 + lr;
-#pragma unroll
-        for (int k = 0; k < KS; ++k) {
-          const bf16x8 kf =
-              *reinterpret_cast<const bf16x8 *>(Ks + key * D + k_swz<D>(2 * k + lh, key) * 8);
-          sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], sacc[b2], 0, 0, 0);
-        }
-      }
-      float mt = -INFINITY;
-#pragma unroll
-      for (int b2 = 0; b2 < 2; ++b2) {
+      for (int b2 = 0; b2 < 2; ++b2)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          float x = sacc[b2][v] * a.scale_log2;
-          if (diag) {
-            const int key = (2 * hf + b2) * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
-            if (key > qrow) x = -INFINITY;
-          }
-          sacc[b2][v] = x;
-          mt = fmaxf(mt, x);
+          const int key = kq + b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
+          if (key > qrow) sacc[b2][v] = -INFINITY;
         }
+    }
+    float mt = -INFINITY;
+#pragma unroll
+    for (int b2 = 0; b2 < 2; ++b2)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sacc[b2][v]);
+    mt = wave_pair_max(mt);
+    // online softmax with the exact running max (the largest weight is exactly 1, which
+    // bf16 holds exactly); the rescale is skipped when no row of the wave has a new max
+    const float m_new = fmaxf(m_ref, mt);
+    if (__ballot(m_new > m_ref)) {
+      const float alpha = __builtin_amdgcn_exp2f((m_ref - m_new) * c);
+      const float a2 = (m_ref == m_new) ? 1.f : alpha;
+      l_run *= a2;
+#pragma unroll
+      for (int i = 0; i < DB; ++i) oacc[i] *= a2;
+      m_ref = m_new;
+    }
+    const float mc = (m_ref == -INFINITY) ? 0.f : m_ref * c;
+    float lsum = 0.f;
+#pragma unroll
+    for (int b2 = 0; b2 < 2; ++b2)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[b2][v], c, -mc));
+        sacc[b2][v] = p;
+        lsum += p;
       }
-      mt = wave_pair_max(mt);
-      const float m_new = fmaxf(m_run, mt);
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-      m_run = m_new;
-      float lsum = 0.f;
-#pragma unroll
-      for (int b2 = 0; b2 < 2; ++b2) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float p = __builtin_amdgcn_exp2f(sacc[b2][v] - m_use);
-          sacc[b2][v] = p;
-          lsum += p;
-        }
-      }
-      l_run = l_run * alpha + lsum;
-#pragma unroll
-      for (int i = 0; i < DB; ++i) oacc[i] *= alpha;
+    l_run += lsum;
 
+    // ---- O^T += V^T P^T over 4 steps of 16 keys; V^T fragments by transposing loads
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const int b2 = ks >> 1;
-        const int half = ks & 1;
-        bf16x8 pf;
+    for (int ks16 = 0; ks16 < 4; ++ks16) {
+      const int b2 = ks16 >> 1;
+      const int half = ks16 & 1;
+      bf16x8 pf;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pf[e] = (__bf16)sacc[b2][8 * half + e];
-        const int unit0 = ((2 * hf + b2) * 32 + 16 * half) / 4 + lh;
+      for (int e = 0; e < 8; ++e) pf[e] = (__bf16)sacc[b2][8 * half + e];
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const int d = db * 32 + lr;
-          const bf16x4 v0 =
-              *reinterpret_cast<const bf16x4 *>(Vt + d * BN + v_swz(unit0, d) * 4);
-          const bf16x4 v1 =
-              *reinterpret_cast<const bf16x4 *>(Vt + d * BN + v_swz(unit0 + 2, d) * 4);
-          const bf16x8 vf = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
-          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, oacc[db], 0, 0, 0);
-        }
+      for (int db = 0; db < DB; ++db) {
+        const int dcol = 32 * db + 16 * (g16 & 1) + 4 * (i16 & 3);
+        const int y = dcol >> 3;
+        const int sub = (dcol & 7) * 2;
+        const int r0 = 16 * ks16 + 4 * (g16 >> 1) + (i16 >> 2);
+        const int r1 = r0 + 8;
+        const s16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4 *)(vs + r0 * S::RB + swz_v<D>(y, r0) * 16 +
+                                                        sub));
+        const s16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4 *)(vs + r1 * S::RB + swz_v<D>(y, r1) * 16 +
+                                                        sub));
+        const s16x8 vv = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pf,
+                                                           oacc[db], 0, 0, 0);
       }
     }
   }
@@ -248,7 +278,6 @@ void sparse_fa_fwd(AttnArgs a) {
     }
   }
 }
-
 
 // number of rows (s, I) with I >= i0, over all sequences
 __device__ __forceinline__ int rows_at_or_above(const SeqTable &st, int i0) {

@@ -269,9 +269,9 @@ def _make_group(spec, s, g, t0, head_set, q, k, v):
     kg = rope(_rng(spec.seed, s, TENSOR_K, g).standard_normal((n, d), dtype=np.float32))
     kg -= (kg @ U) @ U.T
     k_perp = kg.copy()
-    # vertical positions: distinct, uniform in [1, n - b)
-    hi = max(n - b, 2)
-    nv = min(spec.n_vertical, hi - 1)
+    # vertical positions: distinct, uniform in [1, n - b) (none for sequences that short)
+    hi = n - b
+    nv = min(spec.n_vertical, hi - 1) if hi > 1 else 0
     verts = np.sort(srng.choice(np.arange(1, hi), size=nv, replace=False)) if nv > 0 \
         else np.zeros(0, dtype=np.int64)
     if "vs" in kinds:

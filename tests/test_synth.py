@@ -34,15 +34,15 @@ def test_generator_deterministic_and_shaped():
 
 
 def test_generator_varlen_and_partial_heads():
-    spec = synth.SPECS["qwen_varlen"].with_seqlens((300, 129, 1024), name="mini-varlen")
+    spec = synth.SPECS["qwen_varlen"].with_seqlens((300, 129, 1024, 1), name="mini-varlen")
     layer = synth.make_layer(spec, heads=[0, 1])
-    assert layer.q.shape == (1453, 28, 128)
-    assert list(layer.cu_seqlens) == [0, 300, 429, 1453]
+    assert layer.q.shape == (1454, 28, 128)
+    assert list(layer.cu_seqlens) == [0, 300, 429, 1453, 1454]
     assert np.all(layer.q[:, 2:] == 0) and np.any(layer.q[:, :2] != 0)
-    for s in range(3):
+    for s in range(4):
         for g in range(4):
             vs = layer.verticals[s][g]
-            assert np.all((vs >= 1) & (vs < max(spec.seqlens[s] - 128, 2)))
+            assert np.all((vs >= 1) & (vs < spec.seqlens[s] - 128))
 
 
 def test_vertical_slash_structure_is_visible():
