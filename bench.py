@@ -41,8 +41,10 @@ def parse():
     ap.add_argument("--gamma", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
-    ap.add_argument("--cpu-sample-heads", type=int, default=2)
-    ap.add_argument("--cpu-sample-rows", type=int, default=24)
+    ap.add_argument("--cpu-sample-heads", type=int, default=16)
+    ap.add_argument("--cpu-sample-rows", type=int, default=64)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (reference for HBM counters)")
     return ap.parse_args()
 
 
@@ -122,6 +124,14 @@ def main():
     layer = synth.make_layer(spec)
     log(f"[bench] inputs ready in {time.time() - t:.1f}s")
     dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        src = torch.ones(1 << 29, dtype=torch.int16, device=dev)      # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("[bench] copy calibration: 3 x 1 GiB device copies")
+        del src, dst
     q = torch.from_numpy(layer.q).to(torch.bfloat16).to(dev)
     k = torch.from_numpy(layer.k).to(torch.bfloat16).to(dev)
     v = torch.from_numpy(layer.v).to(torch.bfloat16).to(dev)

@@ -33,6 +33,7 @@ fp_status check_shape(const fp_shape *sh, Dims *dm) {
   if (sh->batch > FP_MAX_BATCH) return FP_ERR_UNSUPPORTED;
   if (sh->head_dim != 64 && sh->head_dim != 128) return FP_ERR_UNSUPPORTED;
   if (sh->block != 128) return FP_ERR_UNSUPPORTED;
+  if (sh->num_kv_heads > 1024 || sh->num_q_heads > 8192) return FP_ERR_UNSUPPORTED;
   if (sh->cu_seqlens[0] != 0) return FP_ERR_INVALID_ARG;
   memset(dm, 0, sizeof(*dm));
   fp::SeqTable &st = dm->st;

@@ -71,25 +71,85 @@ __device__ __forceinline__ int swz_v(int y, int r) {
   else return y ^ (((r >> 1) & 1) << 2);
 }
 
-// Issue the DMA of one 64-key stage (keys k0 .. k0+63 of the sequence; rows past the
-// sequence end re-read its last row, they are masked out by the caller).
+// Per-lane byte offsets of the DMA slots of one stage, relative to the stage's first key
+// row: slot i of wave w covers LDS bytes [(4i + w) * 1024, +1024), lane l fills 16 bytes
+// of tile row r with the logical chunk whose swizzled position is the lane's slot.
+template <int D>
+struct DmaOffsets {
+  uint32_t k[Stage<D>::DMA_PER_WAVE];
+  uint32_t v[Stage<D>::DMA_PER_WAVE];
+};
+
+template <int D>
+__device__ __forceinline__ DmaOffsets<D> dma_offsets(uint32_t row_bytes, int w, int lane) {
+  using S = Stage<D>;
+  DmaOffsets<D> o;
+#pragma unroll
+  for (int i = 0; i < S::DMA_PER_WAVE; ++i) {
+    const int r = (i * 4 + w) * S::RPI + lane / S::CPR;
+    const int phys = lane % S::CPR;
+    o.k[i] = r * row_bytes + swz_k<D>(phys, r) * 16;
+    o.v[i] = r * row_bytes + swz_v<D>(phys, r) * 16;
+  }
+  return o;
+}
+
+// Issue the DMA of one 64-key stage: keys k0 .. k0+63 of the sequence through buffer
+// descriptors whose range ends at the last valid key row, so rows past the sequence end
+// read as zeros (and are masked by the caller).
 template <int D>
 __device__ __forceinline__ void stage_dma(uint8_t *ks, uint8_t *vs, const uint16_t *kbase,
                                           const uint16_t *vbase, int64_t kv_row, int k0,
-                                          int kvalid, int w, int lane) {
+                                          int kvalid, const DmaOffsets<D> &off) {
   using S = Stage<D>;
+  const int nrec = (kvalid - 1) * (int)kv_row * 2 + 2 * D;
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc((void *)(kbase + (int64_t)k0 * kv_row), (short)0, nrec,
+                                        0x00020000);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc((void *)(vbase + (int64_t)k0 * kv_row), (short)0, nrec,
+                                        0x00020000);
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
   for (int i = 0; i < S::DMA_PER_WAVE; ++i) {
     const int q = i * 4 + w;
-    const int r = q * S::RPI + lane / S::CPR;
-    const int phys = lane % S::CPR;
-    const int64_t row = (int64_t)(k0 + min(r, kvalid - 1)) * kv_row;
-    __builtin_amdgcn_global_load_lds(
-        (__attribute__((address_space(1))) void *)(kbase + row + swz_k<D>(phys, r) * 8),
-        (__attribute__((address_space(3))) void *)(ks + q * 1024), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(
-        (__attribute__((address_space(1))) void *)(vbase + row + swz_v<D>(phys, r) * 8),
-        (__attribute__((address_space(3))) void *)(vs + q * 1024), 16, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rk, (__attribute__((address_space(3))) void *)(ks + q * 1024), 16, off.k[i], 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rv, (__attribute__((address_space(3))) void *)(vs + q * 1024), 16, off.v[i], 0, 0, 0);
+  }
+}
+
+// One 16-key step of V^T fragments: DB d-blocks x 2 key halves of ds_read_b64_tr_b16.
+// The loads and their lgkmcnt wait are one asm block, so the outputs are only defined
+// once the data has arrived; the compiler's own (conservative) wait for the in-flight
+// DMA of the next stage is thereby avoided.
+template <int DB, int OFF0, int OFF1>
+__device__ __forceinline__ void v_frags(const uint32_t (&addr)[DB], s16x4 (&lo)[DB],
+                                        s16x4 (&hi)[DB]) {
+  if constexpr (DB == 4) {
+    asm volatile(
+        "ds_read_b64_tr_b16 %0, %8 offset:%12\n\t"
+        "ds_read_b64_tr_b16 %1, %8 offset:%13\n\t"
+        "ds_read_b64_tr_b16 %2, %9 offset:%12\n\t"
+        "ds_read_b64_tr_b16 %3, %9 offset:%13\n\t"
+        "ds_read_b64_tr_b16 %4, %10 offset:%12\n\t"
+        "ds_read_b64_tr_b16 %5, %10 offset:%13\n\t"
+        "ds_read_b64_tr_b16 %6, %11 offset:%12\n\t"
+        "ds_read_b64_tr_b16 %7, %11 offset:%13\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(lo[0]), "=&v"(hi[0]), "=&v"(lo[1]), "=&v"(hi[1]), "=&v"(lo[2]), "=&v"(hi[2]),
+          "=&v"(lo[3]), "=&v"(hi[3])
+        : "v"(addr[0]), "v"(addr[1]), "v"(addr[2]), "v"(addr[3]), "i"(OFF0), "i"(OFF1));
+  } else {
+    asm volatile(
+        "ds_read_b64_tr_b16 %0, %4 offset:%6\n\t"
+        "ds_read_b64_tr_b16 %1, %4 offset:%7\n\t"
+        "ds_read_b64_tr_b16 %2, %5 offset:%6\n\t"
+        "ds_read_b64_tr_b16 %3, %5 offset:%7\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(lo[0]), "=&v"(hi[0]), "=&v"(lo[1]), "=&v"(hi[1])
+        : "v"(addr[0]), "v"(addr[1]), "i"(OFF0), "i"(OFF1));
   }
 }
 
@@ -126,8 +186,11 @@ void sparse_fa_fwd(AttnArgs a) {
   const int i16 = lane & 15;
 
   const int cnt = min(a.kb_cnt[(int64_t)h * a.nb_total + a.st.nb_off[s] + I], I + 1);
-  const int32_t *list = a.kb_idx + (int64_t)h * a.tri_total + a.st.tri_off[s] +
-                        (int64_t)I * (I + 1) / 2;
+  // the row's key-block list is read through the scalar cache, one block ahead
+  const __attribute__((address_space(4))) int32_t *list =
+      (const __attribute__((address_space(4))) int32_t *)(a.kb_idx + (int64_t)h * a.tri_total +
+                                                          a.st.tri_off[s] +
+                                                          (int64_t)I * (I + 1) / 2);
 
   // Q^T fragments: lane owns query row q0 + 32w + lr, d = 16k + 8lh .. +8
   constexpr int KS = D / 16;
@@ -151,31 +214,51 @@ void sparse_fa_fwd(AttnArgs a) {
   const int64_t kv_row = (int64_t)a.hkv * D;  // elements between consecutive tokens
   const uint16_t *kbase = a.k + (int64_t)tok0 * kv_row + (int64_t)g * D;
   const uint16_t *vbase = a.v + (int64_t)tok0 * kv_row + (int64_t)g * D;
+  const DmaOffsets<D> doff = dma_offsets<D>((uint32_t)(kv_row * 2), w, lane);
 
   // stage t covers keys J*128 + 64*(t&1) .. +63 of block J = list[t >> 1]
   const int n_stages = 2 * cnt;
-  auto stage_k0 = [&](int t) -> int {
-    const int J = list[t >> 1];
+  auto stage_k0 = [&](int J, int half) -> int {
     if (J < 0 || J > I) return -1;
-    const int k0 = J * BN + 64 * (t & 1);
+    const int k0 = J * BN + 64 * half;
     return k0 < n ? k0 : -1;
   };
+  // per-lane V^T fragment addresses (relative to a V stage), one per d-block
+  uint32_t vaddr_rel[DB];
+  {
+    const int r_l = 4 * (g16 >> 1) + (i16 >> 2);       // row within a 16-key step
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int dcol = 32 * db + 16 * (g16 & 1) + 4 * (i16 & 3);
+      vaddr_rel[db] = r_l * S::RB + swz_v<D>(dcol >> 3, r_l) * 16 + (dcol & 7) * 2;
+    }
+  }
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
 
-  int k0_next = n_stages > 0 ? stage_k0(0) : -1;
+  int J_cur = cnt > 0 ? list[0] : -1;   // block of the stage being prefetched
+  int J_pre = cnt > 1 ? list[1] : -1;   // block after it
+  int k0_next = n_stages > 0 ? stage_k0(J_cur, 0) : -1;
   if (k0_next >= 0)
-    stage_dma<D>(lds, lds + S::BYTES, kbase, vbase, kv_row, k0_next, min(64, n - k0_next), w,
-                 lane);
+    stage_dma<D>(lds, lds + S::BYTES, kbase, vbase, kv_row, k0_next, min(64, n - k0_next), doff);
   for (int t = 0; t < n_stages; ++t) {
     const int k0 = k0_next;
-    uint8_t *ks = lds + (t & 1) * 2 * S::BYTES;
-    uint8_t *vs = ks + S::BYTES;
-    __builtin_amdgcn_s_waitcnt(0);      // this wave's DMA of stage t has landed
+    const int buf = t & 1;
+    uint8_t *ks = lds + buf * 2 * S::BYTES;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's DMA of stage t landed
     __syncthreads();                    // ... and every wave's; stage t-1 reads are done
-    k0_next = (t + 1 < n_stages) ? stage_k0(t + 1) : -1;
+    k0_next = -1;
+    if (t + 1 < n_stages) {
+      if ((t & 1) == 0) {
+        k0_next = stage_k0(J_cur, 1);
+      } else {
+        J_cur = J_pre;
+        J_pre = ((t >> 1) + 2 < cnt) ? list[(t >> 1) + 2] : -1;
+        k0_next = stage_k0(J_cur, 0);
+      }
+    }
     if (k0_next >= 0) {
-      uint8_t *kn = lds + ((t + 1) & 1) * 2 * S::BYTES;
-      stage_dma<D>(kn, kn + S::BYTES, kbase, vbase, kv_row, k0_next, min(64, n - k0_next), w,
-                   lane);
+      uint8_t *kn = lds + (buf ^ 1) * 2 * S::BYTES;
+      stage_dma<D>(kn, kn + S::BYTES, kbase, vbase, kv_row, k0_next, min(64, n - k0_next), doff);
     }
     if (k0 < 0) continue;
 
@@ -234,6 +317,9 @@ void sparse_fa_fwd(AttnArgs a) {
     l_run += lsum;
 
     // ---- O^T += V^T P^T over 4 steps of 16 keys; V^T fragments by transposing loads
+    uint32_t va[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) va[db] = lds_base + (buf * 2 + 1) * S::BYTES + vaddr_rel[db];
 #pragma unroll
     for (int ks16 = 0; ks16 < 4; ++ks16) {
       const int b2 = ks16 >> 1;
@@ -241,20 +327,14 @@ void sparse_fa_fwd(AttnArgs a) {
       bf16x8 pf;
 #pragma unroll
       for (int e = 0; e < 8; ++e) pf[e] = (__bf16)sacc[b2][8 * half + e];
+      s16x4 vlo[DB], vhi[DB];
+      if (ks16 == 0) v_frags<DB, 0 * 16 * S::RB, 0 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
+      if (ks16 == 1) v_frags<DB, 1 * 16 * S::RB, 1 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
+      if (ks16 == 2) v_frags<DB, 2 * 16 * S::RB, 2 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
+      if (ks16 == 3) v_frags<DB, 3 * 16 * S::RB, 3 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const int dcol = 32 * db + 16 * (g16 & 1) + 4 * (i16 & 3);
-        const int y = dcol >> 3;
-        const int sub = (dcol & 7) * 2;
-        const int r0 = 16 * ks16 + 4 * (g16 >> 1) + (i16 >> 2);
-        const int r1 = r0 + 8;
-        const s16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s16x4 *)(vs + r0 * S::RB + swz_v<D>(y, r0) * 16 +
-                                                        sub));
-        const s16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s16x4 *)(vs + r1 * S::RB + swz_v<D>(y, r1) * 16 +
-                                                        sub));
-        const s16x8 vv = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+        const s16x8 vv = __builtin_shufflevector(vlo[db], vhi[db], 0, 1, 2, 3, 4, 5, 6, 7);
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pf,
                                                            oacc[db], 0, 0, 0);
       }
