@@ -32,6 +32,25 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def attn_traffic_bytes(workload):
+    """HBM bytes per attention launch from the committed rocprofv3 counter summary, or None
+    when there is none for this workload or the kernel source has changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "sparse_fa_fwd_traffic.json")
+    src = os.path.join(ROOT, "paper_2502_20766_amd", "csrc", "fp_attn.hip")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+        with open(src, "rb") as f:
+            digest = hashlib.sha256(f.read()).hexdigest()
+    except OSError:
+        return None
+    ent = rec.get("workloads", {}).get(workload)
+    if not ent or rec.get("kernel_source_sha256") != digest:
+        return None
+    return int(ent["hbm_bytes_per_launch"])
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -42,7 +61,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--cpu-sample-heads", type=int, default=16)
-    ap.add_argument("--cpu-sample-rows", type=int, default=64)
+    ap.add_argument("--cpu-sample-rows", type=int, default=32)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM counters)")
     return ap.parse_args()
@@ -234,7 +253,8 @@ def main():
         "speedup_vs_dense": round(dense_ms / ms_step, 3) if dense else None,
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": attn_traffic_bytes(spec.name),
                      "kernel": "sparse_fa_fwd<128>",
                      "per_launch_flop": f_comp},
     }

@@ -1,0 +1,78 @@
+"""Device path vs oracle at the full workload sizes, in the launch configuration the benchmark
+times (same library calls, same shapes).  Block sets are compared for every head and
+sequence; outputs on sampled query blocks (first, last and random rows of every head),
+which the oracle computes one block at a time."""
+import numpy as np
+import pytest
+
+import synth
+from parity import O_MAX_ABS, O_MEAN_ABS, Timer, compare_outputs, compare_selection, log, to_device
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2502_20766_amd as fpx
+    fpx.lib()
+    return fpx
+
+
+CASES = [
+    ("llama3-8b-n32768", "llama32k", None),
+    ("llama3-8b-n131072", "llama128k", None),
+    ("glm4-9b-n65536", "glm64k", None),
+    ("qwen2-7b-varlen-gamma0.9", "qwen_varlen", 0.9),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_fullsize_selection_and_sampled_outputs(case):
+    import paper_2502_20766_amd as fpx
+    name, key, gamma = case
+    spec = synth.SPECS[key]
+    gamma = spec.gamma if gamma is None else gamma
+    log(f"[fullsize] {name}: seqlens={spec.seqlens} hq={spec.hq} hkv={spec.hkv} gamma={gamma} "
+        f"tau={spec.tau} m={spec.min_budget}")
+    with Timer("generate"):
+        layer = synth.make_layer(spec)
+    q, k, v = to_device(layer)
+    with Timer("device select + attention"):
+        idx = fpx.select(q, k, layer.cu_seqlens, gamma, spec.tau, spec.min_budget)
+        o = fpx.sparse_attn(q, k, v, idx)
+        torch.cuda.synchronize()
+    g = dict(masks=fpx.masks_from_indices(idx), pattern=idx.pattern.cpu().numpy(),
+             js=idx.js.cpu().numpy(), units=idx.units.cpu().numpy())
+    o_host = o.float().cpu().numpy()
+    del q, k, v, o
+    with Timer("oracle selection, all heads"):
+        st = compare_selection(layer, g, gamma, spec.tau, spec.min_budget)
+    log(f"  {st}")
+    with Timer("oracle sampled outputs"):
+        mx, mean = compare_outputs(layer, o_host, g["masks"], rows_per_head=4)
+    log(f"  output max_abs {mx:.3e} mean_abs {mean:.3e}")
+    assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
+
+
+@pytest.mark.parametrize("gamma", [0.85, 0.95])
+def test_gamma_sweep_selection_reduced_varlen(gamma):
+    """The gamma sweep of the varlen Qwen-shaped layer, on shortened sequences."""
+    import paper_2502_20766_amd as fpx
+    spec = synth.SPECS["qwen_varlen"].with_seqlens((2048, 4096, 8192, 16384), "qwen-varlen-short")
+    log(f"[gamma sweep] {spec.name} gamma={gamma}")
+    layer = synth.make_layer(spec)
+    q, k, v = to_device(layer)
+    idx = fpx.select(q, k, layer.cu_seqlens, gamma, spec.tau, spec.min_budget)
+    o = fpx.sparse_attn(q, k, v, idx)
+    torch.cuda.synchronize()
+    g = dict(masks=fpx.masks_from_indices(idx), pattern=idx.pattern.cpu().numpy(),
+             js=idx.js.cpu().numpy(), units=idx.units.cpu().numpy())
+    st = compare_selection(layer, g, gamma, spec.tau, spec.min_budget)
+    log(f"  {st}")
+    mx, mean = compare_outputs(layer, o.float().cpu().numpy(), g["masks"], rows_per_head=3)
+    log(f"  output max_abs {mx:.3e} mean_abs {mean:.3e}")
+    assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
