@@ -60,6 +60,7 @@ def parse():
     ap.add_argument("--gamma", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-sdpa", action="store_true", help="skip the PyTorch SDPA dense timing")
     ap.add_argument("--cpu-sample-heads", type=int, default=16)
     ap.add_argument("--cpu-sample-rows", type=int, default=32)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -206,7 +207,7 @@ def main():
         log(f"[bench] dense (library, all blocks) {ms_dense_lib:.3f} ms")
         try:
             import torch.nn.functional as F
-            if len(seqlens) == 1:
+            if len(seqlens) == 1 and not args.no_sdpa:
                 qt = q.transpose(0, 1).unsqueeze(0).contiguous()
                 kt = k.transpose(0, 1).unsqueeze(0).repeat_interleave(
                     spec.hq // spec.hkv, dim=1).contiguous()

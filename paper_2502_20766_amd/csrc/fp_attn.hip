@@ -208,7 +208,7 @@ void sparse_fa_fwd(AttnArgs a) {
 #pragma unroll
   for (int i = 0; i < DB; ++i) oacc[i] = f32x16{};
   float m_ref = -INFINITY;   // reference max (raw logit units) of this lane's row
-  float l_run = 0.f;
+  float l_run = 0.f;          // this lane's share of the row sum (its 32 of 64 keys)
   const float c = a.scale_log2;
 
   const int64_t kv_row = (int64_t)a.hkv * D;  // elements between consecutive tokens
@@ -262,82 +262,119 @@ void sparse_fa_fwd(AttnArgs a) {
     }
     if (k0 < 0) continue;
 
-    // ---- S^T = K Q^T for the stage's 64 keys (2 blocks of 32 keys x 32 queries)
+    // ---- the stage's 64 keys as two 32-key sub-blocks, each an online-softmax step.
+    // Order: S0, S1 on MFMA; max/rescale of 0 and exp of 0 on VALU while S1 runs; max of 1
+    // (rescaling O, l and the fp32 weights of 0 if needed); PV of 0 on MFMA while the exp
+    // of 1 runs on VALU; PV of 1.
+    const int kq = k0 - q0;             // key offset relative to the query block start
+    const bool diag = kq >= 0;          // diagonal block: keys after the query are masked
     f32x16 sacc[2];
-#pragma unroll
-    for (int b2 = 0; b2 < 2; ++b2) {
+    auto qk_block = [&](int b2) {
       sacc[b2] = f32x16{};
       const int r = b2 * 32 + lr;
+      bf16x8 kf[KS];            // all K fragments in flight before the first MFMA
 #pragma unroll
-      for (int k = 0; k < KS; ++k) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(
-            ks + r * S::RB + swz_k<D>(2 * k + lh, r) * 16);
-        sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], sacc[b2], 0, 0, 0);
-      }
-    }
-    // ---- causal mask (diagonal block only) and row max in raw logit units
-    const int kq = k0 - q0;             // key offset relative to the query block start
-    if (kq >= 0) {
-      // diagonal block: keys after this lane's query row get -inf
+      for (int k = 0; k < KS; ++k)
+        kf[k] = *reinterpret_cast<const bf16x8 *>(ks + r * S::RB + swz_k<D>(2 * k + lh, r) * 16);
 #pragma unroll
-      for (int b2 = 0; b2 < 2; ++b2)
+      for (int k = 0; k < KS; ++k)
+        sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[k], qf[k], sacc[b2], 0, 0, 0);
+      // scheduling request: the KS LDS reads first, then the KS MFMAs
+      __builtin_amdgcn_sched_group_barrier(0x100, KS, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, KS, 0);
+    };
+    auto mask_max = [&](int b2) -> float {
+      if (diag) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int key = kq + b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
           if (key > qrow) sacc[b2][v] = -INFINITY;
         }
-    }
-    float mt = -INFINITY;
-#pragma unroll
-    for (int b2 = 0; b2 < 2; ++b2)
+      }
+      float mt = -INFINITY;
 #pragma unroll
       for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sacc[b2][v]);
-    mt = wave_pair_max(mt);
-    // online softmax with the exact running max (the largest weight is exactly 1, which
-    // bf16 holds exactly); the rescale is skipped when no row of the wave has a new max
-    const float m_new = fmaxf(m_ref, mt);
-    if (__ballot(m_new > m_ref)) {
-      const float alpha = __builtin_amdgcn_exp2f((m_ref - m_new) * c);
-      const float a2 = (m_ref == m_new) ? 1.f : alpha;
-      l_run *= a2;
+      return wave_pair_max(mt);
+    };
+    // Move the reference max when some row of the wave sees a new maximum (rare after the
+    // first blocks), rescaling O and the row sums.  Returns whether it moved.
+    auto update_max = [&](float mt) -> bool {
+      const float m_new = fmaxf(m_ref, mt);
+      if (__ballot(m_new > m_ref)) {
+        const float alpha = __builtin_amdgcn_exp2f((m_ref - m_new) * c);
+        const float a2 = (m_ref == m_new) ? 1.f : alpha;
+        l_run *= a2;
 #pragma unroll
-      for (int i = 0; i < DB; ++i) oacc[i] *= a2;
-      m_ref = m_new;
-    }
-    const float mc = (m_ref == -INFINITY) ? 0.f : m_ref * c;
-    float lsum = 0.f;
-#pragma unroll
-    for (int b2 = 0; b2 < 2; ++b2)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[b2][v], c, -mc));
-        sacc[b2][v] = p;
-        lsum += p;
+        for (int i = 0; i < DB; ++i) oacc[i] *= a2;
+        m_ref = m_new;
+        return true;
       }
-    l_run += lsum;
+      return false;
+    };
+    auto weights0 = [&](float (&p0)[16]) {
+      const float mc = (m_ref == -INFINITY) ? 0.f : m_ref * c;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) p0[v] = __builtin_amdgcn_exp2f(fmaf(sacc[0][v], c, -mc));
+    };
+    // sub-block 0 scores and running max
+    qk_block(0);
+    update_max(mask_max(0));
+    // sub-block 1 scores on MFMA while sub-block 0's weights are computed on VALU
+    qk_block(1);
+    float p0[16];
+    weights0(p0);
+    // keep these exponentials here, beside sub-block 1's MFMAs (the compiler would
+    // otherwise sink them past the rescale branch below, next to their use)
+    asm volatile("" : "+v"(p0[0]), "+v"(p0[1]), "+v"(p0[2]), "+v"(p0[3]), "+v"(p0[4]),
+                 "+v"(p0[5]), "+v"(p0[6]), "+v"(p0[7]), "+v"(p0[8]), "+v"(p0[9]),
+                 "+v"(p0[10]), "+v"(p0[11]), "+v"(p0[12]), "+v"(p0[13]), "+v"(p0[14]),
+                 "+v"(p0[15]));
+    // sub-block 1 max; if the reference moved, sub-block 0's weights are recomputed
+    if (update_max(mask_max(1))) weights0(p0);
+    bf16x8 pf0[2];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      pf0[0][e] = (__bf16)p0[e];
+      pf0[1][e] = (__bf16)p0[8 + e];
+      l_run += p0[e] + p0[8 + e];
+    }
 
-    // ---- O^T += V^T P^T over 4 steps of 16 keys; V^T fragments by transposing loads
+    // ---- O^T += V^T P^T, 16 keys per step; V^T fragments by transposing loads
     uint32_t va[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db) va[db] = lds_base + (buf * 2 + 1) * S::BYTES + vaddr_rel[db];
-#pragma unroll
-    for (int ks16 = 0; ks16 < 4; ++ks16) {
-      const int b2 = ks16 >> 1;
-      const int half = ks16 & 1;
-      bf16x8 pf;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) pf[e] = (__bf16)sacc[b2][8 * half + e];
-      s16x4 vlo[DB], vhi[DB];
-      if (ks16 == 0) v_frags<DB, 0 * 16 * S::RB, 0 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
-      if (ks16 == 1) v_frags<DB, 1 * 16 * S::RB, 1 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
-      if (ks16 == 2) v_frags<DB, 2 * 16 * S::RB, 2 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
-      if (ks16 == 3) v_frags<DB, 3 * 16 * S::RB, 3 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
+    auto pv_step = [&](const bf16x8 &pf, s16x4 (&vlo)[DB], s16x4 (&vhi)[DB]) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
         const s16x8 vv = __builtin_shufflevector(vlo[db], vhi[db], 0, 1, 2, 3, 4, 5, 6, 7);
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pf,
                                                            oacc[db], 0, 0, 0);
       }
+    };
+    {
+      s16x4 vlo[DB], vhi[DB];
+      v_frags<DB, 0 * 16 * S::RB, 0 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
+      pv_step(pf0[0], vlo, vhi);
+      v_frags<DB, 1 * 16 * S::RB, 1 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
+      pv_step(pf0[1], vlo, vhi);
+    }
+    // sub-block 1 weights (VALU) overlap the PV MFMAs of sub-block 0
+    bf16x8 pf1[2];
+    {
+      const float mc = (m_ref == -INFINITY) ? 0.f : m_ref * c;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[1][v], c, -mc));
+        pf1[v >> 3][v & 7] = (__bf16)p;
+        l_run += p;
+      }
+    }
+    {
+      s16x4 vlo[DB], vhi[DB];
+      v_frags<DB, 2 * 16 * S::RB, 2 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
+      pv_step(pf1[0], vlo, vhi);
+      v_frags<DB, 3 * 16 * S::RB, 3 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
+      pv_step(pf1[1], vlo, vhi);
     }
   }
 
