@@ -118,7 +118,10 @@ size_t select_layout(const fp_shape *sh, const Dims &dm, char *base, fp::SelectA
   return off;
 }
 
-size_t attn_layout(const Dims &dm) { return align_up(sizeof(int32_t) * dm.nb_total); }
+// attention workspace: row order [Hkv][NB] int32, then 8 queue counters
+size_t attn_layout(const fp_shape *sh, const Dims &dm) {
+  return align_up(sizeof(int32_t) * dm.nb_total * sh->num_kv_heads) + align_up(8 * sizeof(int32_t));
+}
 
 fp_status hip_fail(hipError_t e, const char *what) {
   snprintf(g_last_error, sizeof(g_last_error), "%s: %s", what, hipGetErrorString(e));
@@ -155,7 +158,7 @@ fp_status fp_attn_workspace_size(const fp_shape *shape, size_t *bytes) {
   fp_status st = check_shape(shape, &dm);
   if (st != FP_OK) return st;
   if (!bytes) return FP_ERR_INVALID_ARG;
-  *bytes = attn_layout(dm);
+  *bytes = attn_layout(shape, dm);
   return FP_OK;
 }
 
@@ -168,7 +171,7 @@ fp_status fp_validate(const fp_shape *shape, const fp_params *params, size_t ws_
     const size_t need = params->gamma >= 1.f ? 0 : select_layout(shape, dm, nullptr, nullptr);
     if (ws_bytes < need) return FP_ERR_WORKSPACE;
   } else {
-    if (ws_bytes < attn_layout(dm)) return FP_ERR_WORKSPACE;
+    if (ws_bytes < attn_layout(shape, dm)) return FP_ERR_WORKSPACE;
   }
   return FP_OK;
 }
@@ -247,6 +250,7 @@ fp_status fp_sparse_attn(const fp_shape *shape, const void *q, const void *k, co
       softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
   a.scale_log2 = scale * 1.4426950408889634f;
   a.row_order = (int32_t *)ws;
+  a.queue = (int32_t *)((char *)ws + align_up(sizeof(int32_t) * dm.nb_total * shape->num_kv_heads));
   hipError_t e = fp::launch_sparse_attn(a, (hipStream_t)stream);
   return e == hipSuccess ? FP_OK : hip_fail(e, "fp_sparse_attn");
 }

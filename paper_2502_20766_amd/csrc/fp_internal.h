@@ -82,7 +82,8 @@ struct AttnArgs {
   int32_t nb_total;
   int64_t tri_total;
   float scale_log2;        // softmax scale * log2(e)
-  int32_t *row_order;      // [NB] workspace: dispatch order of (s, I) rows
+  int32_t *row_order;      // [Hkv][NB] workspace: dispatch order of (s, I) rows per KV group
+  int32_t *queue;          // [8] workspace: per-XCD work-queue counters
 };
 
 // Launchers (each returns the hipError_t of its launch).
