@@ -118,9 +118,9 @@ size_t select_layout(const fp_shape *sh, const Dims &dm, char *base, fp::SelectA
   return off;
 }
 
-// attention workspace: row order [Hkv][NB] int32, then 8 queue counters
+// attention workspace: ordered item records [Hq][NB] int4, then 8 queue counters
 size_t attn_layout(const fp_shape *sh, const Dims &dm) {
-  return align_up(sizeof(int32_t) * dm.nb_total * sh->num_kv_heads) + align_up(8 * sizeof(int32_t));
+  return align_up(16 * dm.nb_total * sh->num_q_heads) + align_up(8 * sizeof(int32_t));
 }
 
 fp_status hip_fail(hipError_t e, const char *what) {
@@ -249,8 +249,8 @@ fp_status fp_sparse_attn(const fp_shape *shape, const void *q, const void *k, co
   const float scale =
       softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
   a.scale_log2 = scale * 1.4426950408889634f;
-  a.row_order = (int32_t *)ws;
-  a.queue = (int32_t *)((char *)ws + align_up(sizeof(int32_t) * dm.nb_total * shape->num_kv_heads));
+  a.items = (int4 *)ws;
+  a.queue = (int32_t *)((char *)ws + align_up(16 * dm.nb_total * shape->num_q_heads));
   hipError_t e = fp::launch_sparse_attn(a, (hipStream_t)stream);
   return e == hipSuccess ? FP_OK : hip_fail(e, "fp_sparse_attn");
 }

@@ -18,9 +18,12 @@
 //   * O^T += V^T P^T on the same MFMA: P^T is already in B-operand layout (the key order
 //     inside each 16-key step is permuted identically on both operands), and O^T keeps
 //     one query row per lane, so the rescale by exp2(m_old - m_new) is per lane.
-// Each KV group's rows are dispatched longest first (by the blocks listed for the group's
-// query heads); the G query heads that share a KV head are adjacent in dispatch order
-// and on the same XCD.
+// A persistent grid walks each KV group's (sequence, query head, query block) items in a
+// locality order (longest lists first in buckets, lists that start alike adjacent), every
+// group served by the same XCD(s), so that items running together share K/V tiles in L2.
+#include <algorithm>
+#include <type_traits>
+
 #include "fp_internal.h"
 
 namespace fp {
@@ -95,6 +98,19 @@ __device__ __forceinline__ DmaOffsets<D> dma_offsets(uint32_t row_bytes, int w, 
   return o;
 }
 
+// Buffer descriptor over [base, base + nrec) with out-of-range reads returning zero.  The
+// inputs are made wave-uniform first so the descriptor always lives in scalar registers
+// (a descriptor the compiler believes divergent would be issued once per distinct lane
+// value in a loop).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void *base, int nrec) {
+  const uint64_t p = (uint64_t)(uintptr_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)p);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
+  return __builtin_amdgcn_make_buffer_rsrc((void *)(uintptr_t)(((uint64_t)hi << 32) | lo),
+                                           (short)0, __builtin_amdgcn_readfirstlane(nrec),
+                                           0x00020000);
+}
+
 // Issue the DMA of one 64-key stage: keys k0 .. k0+63 of the sequence through buffer
 // descriptors whose range ends at the last valid key row, so rows past the sequence end
 // read as zeros (and are masked by the caller).
@@ -104,12 +120,8 @@ __device__ __forceinline__ void stage_dma(uint8_t *ks, uint8_t *vs, const uint16
                                           int kvalid, const DmaOffsets<D> &off) {
   using S = Stage<D>;
   const int nrec = (kvalid - 1) * (int)kv_row * 2 + 2 * D;
-  const __amdgpu_buffer_rsrc_t rk =
-      __builtin_amdgcn_make_buffer_rsrc((void *)(kbase + (int64_t)k0 * kv_row), (short)0, nrec,
-                                        0x00020000);
-  const __amdgpu_buffer_rsrc_t rv =
-      __builtin_amdgcn_make_buffer_rsrc((void *)(vbase + (int64_t)k0 * kv_row), (short)0, nrec,
-                                        0x00020000);
+  const __amdgpu_buffer_rsrc_t rk = uniform_rsrc(kbase + (int64_t)k0 * kv_row, nrec);
+  const __amdgpu_buffer_rsrc_t rv = uniform_rsrc(vbase + (int64_t)k0 * kv_row, nrec);
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
   for (int i = 0; i < S::DMA_PER_WAVE; ++i) {
@@ -119,6 +131,22 @@ __device__ __forceinline__ void stage_dma(uint8_t *ks, uint8_t *vs, const uint16
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
         rv, (__attribute__((address_space(3))) void *)(vs + q * 1024), 16, off.v[i], 0, 0, 0);
   }
+}
+
+// Small LDS accesses whose ordering against the in-flight LDS DMA is handled by the
+// caller (so the compiler adds no vmcnt wait of its own).
+__device__ __forceinline__ int lds_read_i32(uint32_t addr) {
+  int v;
+  asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(addr));
+  return v;
+}
+__device__ __forceinline__ int4 lds_read_i32x4(uint32_t addr) {
+  int4 v;
+  asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(addr));
+  return v;
+}
+__device__ __forceinline__ void lds_write_i32(uint32_t addr, int v) {
+  asm volatile("ds_write_b32 %0, %1" ::"v"(addr), "v"(v) : "memory");
 }
 
 // One 16-key step of V^T fragments: DB d-blocks x 2 key halves of ds_read_b64_tr_b16.
@@ -162,24 +190,42 @@ struct Row {
   const __attribute__((address_space(4))) int32_t *list;
 };
 
-// Work item v of XCD x's queue -> (KV group g, query head h, dispatch position pos).
-// Item v of queue x is virtual block vb = 8v + x; the G query heads that share a KV head
-// are adjacent items of one queue, and each KV group's positions follow its
-// longest-first row order.
-struct Item {
-  int g, h, pos;
-};
-__device__ __forceinline__ Item item_of(int vb, int G, int hkv) {
-  const int wg = (vb / (8 * G)) * 8 + (vb % 8);
-  Item it;
-  it.g = wg % hkv;
-  it.h = it.g * G + (vb / 8) % G;
-  it.pos = wg / hkv;
-  return it;
+constexpr int kChunk = 16;   // consecutive ordered items kept together on one XCD
+
+// Item v of XCD x's work queue -> (KV group g, index j into g's ordered items), false once
+// the queue is exhausted (every later v is then exhausted too).
+//  * Hkv divides 8: the 8/Hkv XCDs that share group g = x mod Hkv take its ordered items in
+//    chunks of kChunk, dealt round-robin, so similar items stay on one XCD's L2;
+//  * otherwise XCD x takes the whole lists of groups x, x + 8, ... in turn (XCDs without a
+//    group only steal).
+__device__ __forceinline__ bool queue_item(int x, int v, int hkv, int n_g, int &g, int &j) {
+  if (8 % hkv == 0) {
+    const int r = 8 / hkv;
+    g = x % hkv;
+    j = ((v / kChunk) * r + x / hkv) * kChunk + v % kChunk;
+    return j < n_g;
+  }
+  g = x + 8 * (v / n_g);
+  j = v % n_g;
+  return g < hkv;
 }
-// items in queue x: v with (v / G) * 8 + x < W, W = NB * Hkv
-__device__ __forceinline__ int queue_len(int x, int G, int W) {
-  return W > x ? G * ((W - x + 7) / 8) : 0;
+
+// Item record: {sequence s (6 bits) | query head within the group kk (13) | query block I
+// (13), listed blocks (clamped to I + 1), first listed block, second listed block (-1 when
+// absent)}.
+__device__ __forceinline__ int4 item_record(const SeqTable &st, const int32_t *kb_idx,
+                                            const int32_t *kb_cnt, int nb_total,
+                                            int64_t tri_total, int G, int g, int s, int kk,
+                                            int I) {
+  const int h = g * G + kk;
+  const int cnt = max(0, min(kb_cnt[(int64_t)h * nb_total + st.nb_off[s] + I], I + 1));
+  const int32_t *list = kb_idx + (int64_t)h * tri_total + st.tri_off[s] + (int64_t)I * (I + 1) / 2;
+  int4 r;
+  r.x = (int)(((uint32_t)s << 26) | ((uint32_t)kk << 13) | (uint32_t)I);
+  r.y = cnt;
+  r.z = cnt > 0 ? list[0] : -1;
+  r.w = cnt > 1 ? list[1] : -1;
+  return r;
 }
 
 __device__ __forceinline__ const __attribute__((address_space(4))) int32_t *
@@ -189,6 +235,26 @@ row_list(const AttnArgs &a, int h, int s, int I) {
                                                            (int64_t)I * (I + 1) / 2);
 }
 
+// The same row with every field made wave-uniform (readfirstlane), so that the compiler
+// keeps it in scalar registers whatever control flow it came through.
+__device__ __forceinline__ Row uniform_row(const Row &r) {
+  Row u;
+  u.valid = __builtin_amdgcn_readfirstlane(r.valid);
+  u.I = __builtin_amdgcn_readfirstlane(r.I);
+  u.h = __builtin_amdgcn_readfirstlane(r.h);
+  u.g = __builtin_amdgcn_readfirstlane(r.g);
+  u.cnt = __builtin_amdgcn_readfirstlane(r.cnt);
+  u.tok0 = __builtin_amdgcn_readfirstlane(r.tok0);
+  u.n = __builtin_amdgcn_readfirstlane(r.n);
+  u.J0 = __builtin_amdgcn_readfirstlane(r.J0);
+  u.J1 = __builtin_amdgcn_readfirstlane(r.J1);
+  const uint64_t p = (uint64_t)(uintptr_t)r.list;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)p);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
+  u.list = (const __attribute__((address_space(4))) int32_t *)(uintptr_t)(((uint64_t)hi << 32) | lo);
+  return u;
+}
+
 // First key of stage `half` of key block J in row r, or -1 when the stage has no keys.
 __device__ __forceinline__ int stage_first_key(const Row &r, int J, int half) {
   if (J < 0 || J > r.I) return -1;
@@ -196,14 +262,14 @@ __device__ __forceinline__ int stage_first_key(const Row &r, int J, int half) {
   return k0 < r.n ? k0 : -1;
 }
 
-// Persistent kernel: gridDim.x workgroups, all resident; workgroup b first takes virtual
-// block b (so the first wave of rows is the non-persistent dispatch order), then pulls
-// items from its XCD's queue (x = b % 8, the XCD the hardware places it on) and, once that
-// is empty, from the other XCDs' queues in turn.  The stages of consecutive rows form one
+// Persistent kernel: gridDim.x workgroups, all resident; workgroup b first takes item b / 8
+// of the queue of XCD x = b % 8 (the XCD the hardware places it on), then pulls the next
+// items of that queue through an atomic counter and, once it is empty, those of the other
+// XCDs' queues in turn.  The stages of consecutive rows form one
 // stream: the next row's identity and block list are fetched over the current row's
 // stages (one dependent step per stage, each step's loads covered by the wait for the
-// stage's K/V copy), its first K/V copy is issued at the top of the current row's last
-// stage and its Q fragments load during that stage.
+// stage's K/V copy) and its first K/V copy is issued at the top of the current row's last
+// stage.
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void sparse_fa_fwd(AttnArgs a) {
@@ -212,10 +278,11 @@ void sparse_fa_fwd(AttnArgs a) {
   constexpr int DB = D / 32;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[4 * S::BYTES];  // [2 stages][K, V]
   __shared__ int fetch_slot[2];           // queue positions handed from thread 0 to all
+  __shared__ __attribute__((aligned(16))) int4 rec_slot;   // next row's item record
 
   const int G = a.hq / a.hkv;
-  const int W = a.nb_total * a.hkv;
-  const int P = gridDim.x;                // a multiple of 8G
+  const int n_g = G * a.nb_total;         // items per KV group
+  const int P = gridDim.x;                // a multiple of 8
   const int P8 = P / 8;                   // items per queue taken by the first wave of rows
   const int x0 = blockIdx.x & 7;
   const int tid = threadIdx.x;
@@ -229,91 +296,114 @@ void sparse_fa_fwd(AttnArgs a) {
   const float c = a.scale_log2;
   const int64_t kv_row = (int64_t)a.hkv * D;  // elements between consecutive tokens
 
-  // ---- first row: virtual block b, read directly
+  // a row from its item record {packed (s, kk, I), blocks, first block, second block}
+  auto row_from = [&](int g, int32_t packed, int cnt, int j0, int j1) {
+    Row r;
+    const int s = (uint32_t)packed >> 26;
+    r.valid = 1;
+    r.g = g;
+    r.h = g * G + ((packed >> 13) & 0x1FFF);
+    r.I = packed & 0x1FFF;
+    r.tok0 = a.st.cu[s];
+    r.n = a.st.cu[s + 1] - r.tok0;
+    r.cnt = cnt;
+    r.J0 = j0;
+    r.J1 = j1;
+    r.list = row_list(a, r.h, s, r.I);
+    return r;
+  };
+
+  // ---- first row: item blockIdx / 8 of this XCD's queue, read directly
   Row cur;
+  cur.valid = 0;
   {
-    const int vb = blockIdx.x;
-    if ((vb / (8 * G)) * 8 + (vb % 8) >= W) return;
-    const Item it = item_of(vb, G, a.hkv);
-    const int packed = a.row_order[(int64_t)it.g * a.nb_total + it.pos];
-    cur.valid = 1;
-    cur.g = it.g;
-    cur.h = it.h;
-    const int s = packed >> 20;
-    cur.I = packed & 0xFFFFF;
-    cur.tok0 = a.st.cu[s];
-    cur.n = a.st.cu[s + 1] - cur.tok0;
-    cur.cnt = min(a.kb_cnt[(int64_t)cur.h * a.nb_total + a.st.nb_off[s] + cur.I], cur.I + 1);
-    cur.list = row_list(a, cur.h, s, cur.I);
-    cur.J0 = cur.cnt > 0 ? cur.list[0] : -1;
-    cur.J1 = cur.cnt > 1 ? cur.list[1] : -1;
+    int g, j;
+    if (queue_item(x0, blockIdx.x >> 3, a.hkv, n_g, g, j)) {
+      const int4 rec = a.items[(int64_t)g * n_g + j];
+      cur = row_from(g, __builtin_amdgcn_readfirstlane(rec.x), __builtin_amdgcn_readfirstlane(rec.y),
+                     __builtin_amdgcn_readfirstlane(rec.z), __builtin_amdgcn_readfirstlane(rec.w));
+    }
   }
 
-  // ---- next-row fetch: a small state machine advanced once per stage
-  //   fs 0: take a queue position (atomic by thread 0)        -> fs 1
-  //   fs 1: position known; empty queue -> next queue (fs 1), else load row_order -> fs 2
-  //   fs 2: (s, I) known; load the count and first two list entries      -> fs 3
-  //   fs 3: row complete                                                  -> fs 4
+  // ---- next-row fetch, spread over the current row:
+  //   row setup: thread 0 takes a queue position (atomic), retired with the row's Q loads
+  //              and published in LDS                                       -> fs 1
+  //   fs 1 (first stage top, after the barrier): position known; if that queue is empty,
+  //         positions of the next queues are taken right away; else lanes 0-3 of wave 0
+  //         copy the item record into LDS (LDS DMA)                         -> fs 2
+  //   fs 2 (next stage top, covered by its wait and barrier): next row complete -> fs 4
+  // No load result stays in flight in a register across the stage loop (the compiler
+  // would otherwise wait for it, and with it for the K/V DMA, inside the stages).
   Row nxt;
   nxt.valid = 0;
-  int fs = 0, qi = 0, n_fetch = 0;
-  int ret_atomic = 0, ret_row = 0, ret_cnt = 0, ret_j0 = 0, ret_j1 = 0;
-  auto fetch_issue = [&]() {
-    if (tid == 0) ret_atomic = atomicAdd(a.queue + ((x0 + qi) & 7), 1);
+  int fs = 4, qi = 0, n_fetch = 0, fetch_g = 0;
+  const uint32_t rec_off = 4u * (uint32_t)(tid & 3);   // record dword of lanes 0-3
+  const uint32_t slot_addr =
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int *)fetch_slot;
+  const uint32_t rec_addr =
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int4 *)&rec_slot;
+  // workgroup barrier without a memory fence: the callers wait for exactly the memory
+  // operations the other waves depend on (LDS DMA by vmcnt, LDS writes by lgkmcnt)
+  auto barrier = [&]() {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
   };
-  // thread 0 publishes the position it received; runs before a barrier
-  auto fetch_publish = [&]() {
-    if (fs == 1 && tid == 0) fetch_slot[n_fetch & 1] = ret_atomic;
+  // thread 0 takes the next position of queue (x0 + qi) and publishes it in slot n_fetch;
+  // the atomic's return is consumed at once (the caller places this where a wait is paid
+  // anyway)
+  auto take_position = [&]() {
+    if (tid == 0) {
+      const int p = atomicAdd(a.queue + ((x0 + qi) & 7), 1);
+      lds_write_i32(slot_addr + 4 * (n_fetch & 1), p);
+    }
+    // the fetch state stays wave-uniform across the thread-0 branch above
+    qi = __builtin_amdgcn_readfirstlane(qi);
+    n_fetch = __builtin_amdgcn_readfirstlane(n_fetch);
   };
-  // one step; call after a barrier that follows fetch_publish
+  // one step; call after a barrier that follows the publication of slot n_fetch
   auto fetch_step = [&]() {
-    if (fs == 0) {
-      fetch_issue();
-      fs = 1;
-    } else if (fs == 1) {
-      const int x = (x0 + qi) & 7;
-      const int v = P8 + __builtin_amdgcn_readfirstlane(fetch_slot[n_fetch & 1]);
-      ++n_fetch;
-      if (v >= queue_len(x, G, W)) {
-        if (++qi == 8) {
-          fs = 4;                       // every queue drained: no next row
-        } else {
-          fetch_issue();
+    if (fs == 1) {
+      while (true) {
+        const int x = (x0 + qi) & 7;
+        const int v =
+            P8 + __builtin_amdgcn_readfirstlane(lds_read_i32(slot_addr + 4 * (n_fetch & 1)));
+        ++n_fetch;
+        int g, j;
+        if (queue_item(x, v, a.hkv, n_g, g, j)) {
+          fetch_g = g;
+          if (tid < 4) {
+            const __amdgpu_buffer_rsrc_t rr = uniform_rsrc(a.items + (int64_t)g * n_g + j, 16);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rr, (__attribute__((address_space(3))) void *)&rec_slot, 4, rec_off, 0, 0, 0);
+          }
+          fs = 2;
+          fetch_g = __builtin_amdgcn_readfirstlane(fetch_g);
+          n_fetch = __builtin_amdgcn_readfirstlane(n_fetch);
+          qi = __builtin_amdgcn_readfirstlane(qi);
+          break;
         }
-      } else {
-        const Item it = item_of(8 * v + x, G, a.hkv);
-        nxt.g = it.g;
-        nxt.h = it.h;
-        ret_row = *(a.row_order + (int64_t)it.g * a.nb_total + it.pos);
-        fs = 2;
+        if (++qi == 8) {                // every queue drained: no next row
+          fs = 4;
+          break;
+        }
+        take_position();                // rare: this queue is empty, try the next one now
+        barrier();
       }
     } else if (fs == 2) {
-      const int packed = __builtin_amdgcn_readfirstlane(ret_row);
-      const int s = packed >> 20;
-      nxt.I = packed & 0xFFFFF;
-      nxt.tok0 = a.st.cu[s];
-      nxt.n = a.st.cu[s + 1] - nxt.tok0;
-      nxt.list = row_list(a, nxt.h, s, nxt.I);
-      const int32_t *lv = (const int32_t *)nxt.list;
-      ret_cnt = a.kb_cnt[(int64_t)nxt.h * a.nb_total + a.st.nb_off[s] + nxt.I];
-      ret_j0 = lv[0];
-      ret_j1 = lv[nxt.I > 0 ? 1 : 0];   // list of block I has I + 1 slots
-      fs = 3;
-    } else if (fs == 3) {
-      nxt.cnt = min(__builtin_amdgcn_readfirstlane(ret_cnt), nxt.I + 1);
-      nxt.J0 = nxt.cnt > 0 ? __builtin_amdgcn_readfirstlane(ret_j0) : -1;
-      nxt.J1 = nxt.cnt > 1 ? __builtin_amdgcn_readfirstlane(ret_j1) : -1;
-      nxt.valid = 1;
+      const int4 rec = lds_read_i32x4(rec_addr);
+      nxt = row_from(fetch_g, __builtin_amdgcn_readfirstlane(rec.x),
+                     __builtin_amdgcn_readfirstlane(rec.y), __builtin_amdgcn_readfirstlane(rec.z),
+                     __builtin_amdgcn_readfirstlane(rec.w));
       fs = 4;
     }
   };
   // complete the fetch now (rows with fewer stages than fetch steps)
   auto fetch_finish = [&]() {
     while (fs < 4) {
-      if (fs == 1) {
+      if (fs == 2) {
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        fetch_publish();
-        __syncthreads();
+        barrier();
       }
       fetch_step();
     }
@@ -336,6 +426,11 @@ void sparse_fa_fwd(AttnArgs a) {
       vaddr_rel[db] = r_l * S::RB + swz_v<D>(dcol >> 3, r_l) * 16 + (dcol & 7) * 2;
     }
   }
+  // per-lane K fragment addresses (relative to a K stage) of sub-block 0; sub-block 1 is
+  // 32 rows further (the swizzles repeat every 32 rows)
+  uint32_t kaddr_rel[KS];
+#pragma unroll
+  for (int k = 0; k < KS; ++k) kaddr_rel[k] = lr * S::RB + swz_k<D>(2 * k + lh, lr) * 16;
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
   auto issue = [&](const Row &r, int k0, int into) {
     const uint16_t *kb = a.k + (int64_t)r.tok0 * kv_row + (int64_t)r.g * D;
@@ -344,16 +439,34 @@ void sparse_fa_fwd(AttnArgs a) {
     stage_dma<D>(dst, dst + S::BYTES, kb, vbp, kv_row, k0, min(64, r.n - k0), doff);
   };
 
+  if (!cur.valid) {                       // this XCD's queue had no first item: take one
+    take_position();
+    fs = 1;
+    barrier();
+    fetch_finish();
+    if (!nxt.valid) return;
+    cur = nxt;
+    nxt.valid = 0;
+  }
   int buf = 0;
   int k0_next = stage_first_key(cur, cur.J0, 0);
   if (k0_next >= 0) issue(cur, k0_next, buf);
   bf16x8 qf[KS];
-  bool q_ready = false;
   while (true) {
     // ---- row setup: Q^T fragments (lane owns query row q0 + qrow), zero state
+    cur = uniform_row(cur);
     const int q0 = cur.I * BM;
-    if (!q_ready) load_q(cur, qf);
-    q_ready = false;
+    // the next row's queue position and this row's Q fragments load together, and both are
+    // retired here: the stage loop then holds no pending register load, so the compiler
+    // adds no wait before its MFMAs (which would also wait for the K/V DMA)
+    if (qi < 8) {
+      take_position();
+      fs = 1;
+    }
+    fs = __builtin_amdgcn_readfirstlane(fs);
+    load_q(cur, qf);
+#pragma unroll
+    for (int k = 0; k < KS; ++k) asm volatile("" : "+v"(qf[k]));
     f32x16 oacc[DB];
 #pragma unroll
     for (int i = 0; i < DB; ++i) oacc[i] = f32x16{};
@@ -368,8 +481,7 @@ void sparse_fa_fwd(AttnArgs a) {
       const int k0 = k0_next;
       const uint8_t *ks = lds + buf * 2 * S::BYTES;
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's DMA of stage t landed
-      fetch_publish();
-      __syncthreads();                  // ... and every wave's; stage t-1 reads are done
+      barrier();                        // ... and every wave's; stage t-1 reads are done
       fetch_step();
       // the next stage is the row's next one, or the first stage of the next row
       k0_next = -1;
@@ -394,20 +506,20 @@ void sparse_fa_fwd(AttnArgs a) {
 
     const int kq = k0 - q0;             // key offset relative to the query block start
     const bool diag = kq >= 0;          // diagonal block: keys after the query are masked
+    uint32_t ka[KS];                    // this stage's K fragment LDS addresses (sub-block 0)
+#pragma unroll
+    for (int k = 0; k < KS; ++k) ka[k] = lds_base + (buf ^ 1) * 2 * S::BYTES + kaddr_rel[k];
     f32x16 sacc[2];
-    auto qk_block = [&](int b2) {
+    auto qk_block = [&](auto b2c) {
+      constexpr int b2 = decltype(b2c)::value;
       sacc[b2] = f32x16{};
-      const int r = b2 * 32 + lr;
       bf16x8 kf[KS];            // all K fragments in flight before the first MFMA
 #pragma unroll
       for (int k = 0; k < KS; ++k)
-        kf[k] = *reinterpret_cast<const bf16x8 *>(ks + r * S::RB + swz_k<D>(2 * k + lh, r) * 16);
+        kf[k] = *reinterpret_cast<const bf16x8 *>(lds + (ka[k] - lds_base) + b2 * 32 * S::RB);
 #pragma unroll
       for (int k = 0; k < KS; ++k)
         sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[k], qf[k], sacc[b2], 0, 0, 0);
-      // scheduling request: the KS LDS reads first, then the KS MFMAs
-      __builtin_amdgcn_sched_group_barrier(0x100, KS, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, KS, 0);
     };
     auto mask_max = [&](int b2) -> float {
       if (diag) {
@@ -443,16 +555,10 @@ void sparse_fa_fwd(AttnArgs a) {
       for (int v = 0; v < 16; ++v) p0[v] = __builtin_amdgcn_exp2f(fmaf(sacc[0][v], c, -mc));
     };
     // sub-block 0 scores and running max
-    qk_block(0);
+    qk_block(std::integral_constant<int, 0>{});
     update_max(mask_max(0));
     // sub-block 1 scores on MFMA while sub-block 0's weights are computed on VALU
-    qk_block(1);
-    // last stage of the row: the next row's Q fragments replace this row's (their last use
-    // was the MFMAs just issued) and load while this stage finishes
-    if (t + 1 == n_stages && nxt.valid) {
-      load_q(nxt, qf);
-      q_ready = true;
-    }
+    qk_block(std::integral_constant<int, 1>{});
     float p0[16];
     weights0(p0);
     // keep these exponentials here, beside sub-block 1's MFMAs (the compiler would
@@ -530,7 +636,6 @@ void sparse_fa_fwd(AttnArgs a) {
     if (!nxt.valid) break;
     cur = nxt;
     nxt.valid = 0;
-    fs = 0;
   }
 }
 
@@ -544,10 +649,25 @@ __device__ __forceinline__ int rows_at_or_above(const SeqTable &st, int i0) {
   return c;
 }
 
-// Fallback dispatch order (query block descending, then sequence ascending), used when a
-// group has too many rows for the in-LDS sort; entry = (s << 20) | I, same for every group.
-__global__ void build_row_order(SeqTable st, int hkv, int32_t *row_order, int32_t *queue) {
+// sequence holding global row r (nb_off ascending, n_seq <= 64)
+__device__ __forceinline__ int seq_of_row(const SeqTable &st, int r) {
+  int lo = 0, hi = st.n_seq;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (st.nb_off[mid] <= r) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+// Plain item order, used when a group has too many items for the in-LDS sort: rows by query
+// block descending (then sequence ascending), the G heads of a row adjacent.  Same for every
+// group.  Also resets the queue counters.
+__global__ void build_item_order_plain(SeqTable st, const int32_t *kb_idx, const int32_t *kb_cnt,
+                                       int hq, int hkv, int64_t tri_total, int4 *items,
+                                       int32_t *queue) {
   const int nb_total = st.nb_off[st.n_seq];
+  const int G = hq / hkv;
+  const int64_t n_g = (int64_t)G * nb_total;
   if (blockIdx.x == 0 && threadIdx.x < 8) queue[threadIdx.x] = 0;
   for (int pos = blockIdx.x * blockDim.x + threadIdx.x; pos < nb_total;
        pos += gridDim.x * blockDim.x) {
@@ -565,75 +685,93 @@ __global__ void build_row_order(SeqTable st, int hkv, int32_t *row_order, int32_
         --idx;
       }
     }
-    for (int g = 0; g < hkv; ++g) row_order[(int64_t)g * nb_total + pos] = (s << 20) | lo;
+    for (int g = 0; g < hkv; ++g)
+      for (int kk = 0; kk < G; ++kk)
+        items[g * n_g + (int64_t)pos * G + kk] =
+            item_record(st, kb_idx, kb_cnt, nb_total, tri_total, G, g, s, kk, lo);
   }
 }
 
-constexpr int kSortMax = 8192;   // rows per KV group sorted in LDS
+constexpr int kSortItems = 16384;   // items per KV group sorted in LDS (128 KB of keys)
 
-// Longest-processing-time-first order of one KV group's rows: cost = blocks listed for
-// the row summed over the group's query heads; ties by query block descending.
-__global__ __launch_bounds__(1024) void build_row_order_lpt(SeqTable st, const int32_t *kb_cnt,
-                                                            int hq, int hkv,
-                                                            int32_t *row_order,
-                                                            int32_t *queue) {
-  __shared__ unsigned long long key[kSortMax];
+// Locality order of one KV group's items (s, head, I): ascending by
+//   [1023 - min(blocks / 4, 1023)] [first three listed blocks after block 0] [item id],
+// i.e. longest first in buckets of 4 blocks, and inside a bucket items whose lists start
+// alike are adjacent, so that the items running at the same time on an XCD read the same
+// K/V tiles through its L2.  Item id = row * G + kk (heads of a row adjacent).  Also resets
+// the queue counters.
+__global__ __launch_bounds__(1024) void build_item_order_sorted(SeqTable st, const int32_t *kb_idx,
+                                                                const int32_t *kb_cnt, int hq,
+                                                                int hkv, int64_t tri_total,
+                                                                int4 *items, int32_t *queue) {
+  __shared__ unsigned long long key[kSortItems];
   const int g = blockIdx.x;
   const int G = hq / hkv;
   const int nb_total = st.nb_off[st.n_seq];
+  const int n_g = G * nb_total;
   if (g == 0 && threadIdx.x < 8) queue[threadIdx.x] = 0;
   int np = 1;
-  while (np < nb_total) np <<= 1;
-  for (int r = threadIdx.x; r < np; r += blockDim.x) {
-    unsigned long long kv = 0ull;               // padding sorts last
-    if (r < nb_total) {
-      int s = 0;
-      while (s + 1 < st.n_seq && st.nb_off[s + 1] <= r) ++s;
+  while (np < n_g) np <<= 1;
+  for (int id = threadIdx.x; id < np; id += blockDim.x) {
+    unsigned long long kv = ~0ull;               // padding sorts last
+    if (id < n_g) {
+      const int r = id / G, kk = id % G;
+      const int s = seq_of_row(st, r);
       const int I = r - st.nb_off[s];
-      unsigned cost = 0;
-      for (int k = 0; k < G; ++k) cost += (unsigned)kb_cnt[(int64_t)(g * G + k) * nb_total + r];
-      kv = ((unsigned long long)(cost + 1) << 40) | ((unsigned long long)I << 20) |
-           (unsigned long long)(0xFFFFF - s);
+      const int h = g * G + kk;
+      const int cnt = max(0, min(kb_cnt[(int64_t)h * nb_total + r], I + 1));
+      const int32_t *list = kb_idx + (int64_t)h * tri_total + st.tri_off[s] + (int64_t)I * (I + 1) / 2;
+      unsigned long long e[3];
+#pragma unroll
+      for (int t = 0; t < 3; ++t)
+        e[t] = cnt > t + 1 ? min((unsigned)list[t + 1], 0x1FFFu) : 0x1FFFu;
+      const unsigned long long bucket = (unsigned long long)min(cnt >> 2, 1023);
+      kv = ((1023ull - bucket) << 53) | (e[0] << 40) | (e[1] << 27) | (e[2] << 14) |
+           (unsigned long long)id;
     }
-    key[r] = kv;
+    key[id] = kv;
   }
   __syncthreads();
-  // bitonic sort, descending
+  // bitonic sort, ascending
   for (int size = 2; size <= np; size <<= 1) {
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
       for (int i = threadIdx.x; i < np; i += blockDim.x) {
         const int j = i ^ stride;
         if (j > i) {
-          const bool desc = (i & size) == 0;
-          const unsigned long long a = key[i], b = key[j];
-          if (desc ? (a < b) : (a > b)) {
-            key[i] = b;
-            key[j] = a;
+          const bool up = (i & size) == 0;
+          const unsigned long long x = key[i], y = key[j];
+          if (up ? (x > y) : (x < y)) {
+            key[i] = y;
+            key[j] = x;
           }
         }
       }
       __syncthreads();
     }
   }
-  for (int r = threadIdx.x; r < nb_total; r += blockDim.x) {
-    const unsigned long long kv = key[r];
-    const int I = (int)((kv >> 20) & 0xFFFFF);
-    const int s = 0xFFFFF - (int)(kv & 0xFFFFF);
-    row_order[(int64_t)g * nb_total + r] = (s << 20) | I;
+  for (int t = threadIdx.x; t < n_g; t += blockDim.x) {
+    const int id = (int)(key[t] & 0x3FFF);
+    const int r = id / G, kk = id % G;
+    const int s = seq_of_row(st, r);
+    items[(int64_t)g * n_g + t] =
+        item_record(st, kb_idx, kb_cnt, nb_total, tri_total, G, g, s, kk, r - st.nb_off[s]);
   }
 }
 
 }  // namespace
 
 hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t stream) {
-  if (a.nb_total <= kSortMax)
-    hipLaunchKernelGGL(build_row_order_lpt, dim3(a.hkv), dim3(1024), 0, stream, a.st, a.kb_cnt,
-                       a.hq, a.hkv, a.row_order, a.queue);
+  const int G = a.hq / a.hkv;
+  const int64_t n_g = (int64_t)G * a.nb_total;
+  if (n_g <= kSortItems)
+    hipLaunchKernelGGL(build_item_order_sorted, dim3(a.hkv), dim3(1024), 0, stream, a.st,
+                       a.kb_idx, a.kb_cnt, a.hq, a.hkv, a.tri_total, a.items, a.queue);
   else
-    hipLaunchKernelGGL(build_row_order, dim3((a.nb_total + 255) / 256), dim3(256), 0, stream,
-                       a.st, a.hkv, a.row_order, a.queue);
-  // Persistent grid: about two resident workgroups per CU, a multiple of 8G so that every
-  // block stays on one XCD's share of KV groups and the G heads of a row run together.
+    hipLaunchKernelGGL(build_item_order_plain, dim3((a.nb_total + 255) / 256), dim3(256), 0,
+                       stream, a.st, a.kb_idx, a.kb_cnt, a.hq, a.hkv, a.tri_total, a.items,
+                       a.queue);
+  // Persistent grid: two resident workgroups per CU (a multiple of 8, one share per XCD),
+  // no more than there are items.
   static int cus = 0;
   if (cus == 0) {
     int dev = 0;
@@ -642,11 +780,8 @@ hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t stream) {
         cus <= 0)
       cus = 256;
   }
-  const int G = a.hq / a.hkv;
-  const int unit = 8 * G;
-  const int total = ((a.nb_total * a.hkv + 7) / 8) * unit;
-  int blocks = max(unit, (2 * cus / unit) * unit);
-  blocks = min(blocks, total);
+  const int64_t total = n_g * a.hkv;
+  const int blocks = (int)std::min<int64_t>((2 * cus / 8) * 8, (total + 7) / 8 * 8);
   if (a.d == 128)
     hipLaunchKernelGGL(sparse_fa_fwd<128>, dim3(blocks), dim3(kThreads), 0, stream, a);
   else

@@ -82,7 +82,7 @@ struct AttnArgs {
   int32_t nb_total;
   int64_t tri_total;
   float scale_log2;        // softmax scale * log2(e)
-  int32_t *row_order;      // [Hkv][NB] workspace: dispatch order of (s, I) rows per KV group
+  int4 *items;             // [Hkv][G * NB] workspace: ordered item records per KV group
   int32_t *queue;          // [8] workspace: per-XCD work-queue counters
 };
 
