@@ -25,9 +25,13 @@ from .flexprefill import (  # noqa: F401
     vertical_slash_index,
     query_aware_block_attention,
     query_aware_index,
+    query_aware_index_rows,
     tiles_from_vertical_slash,
     tiles_from_query_aware,
+    tiles_from_query_aware_rows,
     add_forced_and_min_budget,
+    row_priority,
+    apply_max_budget,
     select_head,
     select,
     sparse_attention_rows,

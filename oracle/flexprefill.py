@@ -29,6 +29,15 @@ Readings taken where the paper is silent (each is also listed in the design note
       full attention).
   R10 Pooling windows are aligned to token 0 of each sequence; a partial last window is
       averaged over its own tokens.
+  R11 The query-wise alternative to the flatten step of Algorithm 4 (appendix "flatten
+      ablation": the selected key blocks of each query block reach gamma): every query
+      block I is its own selection problem over the key blocks J <= I, scored by
+      A_bar[I, J] divided by the row's sum, with the rule of R6.
+  R12 The maximum computational budget (appendix "maximum budget limit") is a cap of M
+      key blocks per query-block row, applied after R8: a row with more than M blocks
+      keeps blocks 0 and I and then its other blocks in the order R8 uses to add them
+      (pooled score for query-aware heads, nearest to the diagonal for vertical-slash
+      heads).  M = 0 means no cap.
 """
 from __future__ import annotations
 
@@ -252,6 +261,25 @@ def query_aware_index(a_bar_map: np.ndarray, gamma: float):
     return sel, unit_ids
 
 
+def query_aware_index_rows(a_bar_map: np.ndarray, gamma: float):
+    """Query-wise variant of Algorithm 4 (R11): for each query block I, the key blocks
+    J <= I scored by A_bar[I, J] / sum_J A_bar[I, J], argsorted, and the minimal prefix with
+    mass >= gamma.  Returns one Selection per query block (unit id = J)."""
+    nb = a_bar_map.shape[0]
+    sels = []
+    for I in range(nb):
+        row = a_bar_map[I, :I + 1]
+        sels.append(cumulative_select(row / np.sum(row), gamma))
+    return sels
+
+
+def tiles_from_query_aware_rows(sels, nb: int) -> np.ndarray:
+    mask = np.zeros((nb, nb), dtype=bool)
+    for I, sel in enumerate(sels):
+        mask[I, sel.selected] = True
+    return mask
+
+
 def tiles_from_query_aware(selected_units: np.ndarray, nb: int) -> np.ndarray:
     mask = np.zeros((nb, nb), dtype=bool)
     su = np.asarray(selected_units, dtype=np.int64)
@@ -288,12 +316,46 @@ def add_forced_and_min_budget(mask: np.ndarray, pattern: int, min_budget: int,
     return mask
 
 
+def row_priority(I: int, pattern: int, a_bar_map: np.ndarray | None = None) -> np.ndarray:
+    """Key blocks of row I in the order R8 adds them and R12 keeps them: pooled score
+    descending then J ascending (query-aware), or nearest to the diagonal first
+    (vertical-slash)."""
+    if pattern == PATTERN_QA:
+        cand = np.arange(I + 1)
+        return cand[np.lexsort((cand, -a_bar_map[I, :I + 1]))]
+    return np.arange(I, -1, -1)
+
+
+def apply_max_budget(mask: np.ndarray, pattern: int, max_budget: int,
+                     a_bar_map: np.ndarray | None = None) -> np.ndarray:
+    """Cap every row at max_budget key blocks (R12): blocks 0 and I first, then the row's
+    other blocks in row_priority order.  max_budget <= 0 leaves the mask unchanged."""
+    if max_budget <= 0:
+        return mask
+    mask = mask.copy()
+    nb = mask.shape[0]
+    for I in range(nb):
+        if int(np.count_nonzero(mask[I, :I + 1])) <= max_budget:
+            continue
+        keep = {0, I}
+        for J in row_priority(I, pattern, a_bar_map):
+            if len(keep) >= max_budget:
+                break
+            if mask[I, J]:
+                keep.add(int(J))
+        mask[I, :] = False
+        mask[I, sorted(keep)] = True
+    return mask
+
+
 # ------------------------------------------------------------------ Algorithm 1 selection part
 
 def select_head(q_seq, k_seq, block, gamma, tau, min_budget, scale, force_pattern=-1,
-                keep_detail=False):
+                keep_detail=False, max_budget=0, qa_mode=0):
     """Pattern search and index selection for one head of one sequence (Algorithm 1 up to
-    the final attention).  Returns a dict with pattern, d_js, tile mask and counts."""
+    the final attention).  qa_mode 0 selects query-aware units over the flattened map
+    (Algorithm 4), 1 per query block (R11); max_budget caps the rows (R12).  Returns a
+    dict with pattern, d_js, tile mask and counts."""
     n = q_seq.shape[0]
     nb = -(-n // block)
     if gamma >= 1.0:                                          # R9
@@ -307,16 +369,25 @@ def select_head(q_seq, k_seq, block, gamma, tau, min_budget, scale, force_patter
     detail = dict(a_bar=a_bar, a_blk=a_blk) if keep_detail else None
     if pattern == PATTERN_QA:
         a_map = query_aware_block_attention(q_seq, k_seq, block, scale)
-        sel, unit_ids = query_aware_index(a_map, gamma)
-        mask = tiles_from_query_aware(unit_ids[sel.selected], nb)
+        if qa_mode == 1:
+            row_sels = query_aware_index_rows(a_map, gamma)
+            mask = tiles_from_query_aware_rows(row_sels, nb)
+            units = (sum(sl.k for sl in row_sels), 0)
+            if keep_detail:
+                detail.update(qa_rows=row_sels, a_map=a_map)
+        else:
+            sel, unit_ids = query_aware_index(a_map, gamma)
+            mask = tiles_from_query_aware(unit_ids[sel.selected], nb)
+            units = (sel.k, 0)
+            if keep_detail:
+                detail.update(qa=sel, unit_ids=unit_ids, a_map=a_map)
         mask = add_forced_and_min_budget(mask, PATTERN_QA, min_budget, a_map)
-        units = (sel.k, 0)
-        if keep_detail:
-            detail.update(qa=sel, unit_ids=unit_ids, a_map=a_map)
+        mask = apply_max_budget(mask, PATTERN_QA, max_budget, a_map)
     else:
         sel_v, sel_s, a_v, a_s = vertical_slash_index(a_full, rows, gamma)
         mask = tiles_from_vertical_slash(sel_v.selected, sel_s.selected, n, block)
         mask = add_forced_and_min_budget(mask, PATTERN_VS, min_budget)
+        mask = apply_max_budget(mask, PATTERN_VS, max_budget)
         units = (sel_v.k, sel_s.k)
         if keep_detail:
             detail.update(v=sel_v, s=sel_s, a_v=a_v, a_s=a_s)
@@ -324,7 +395,7 @@ def select_head(q_seq, k_seq, block, gamma, tau, min_budget, scale, force_patter
 
 
 def select(q, k, cu_seqlens, block, gamma, tau, min_budget, scale=None, force_pattern=None,
-           heads=None, keep_detail=False):
+           heads=None, keep_detail=False, max_budget=0, qa_mode=0):
     """Selection for a packed layer.  q: [T, Hq, d], k: [T, Hkv, d].  Returns a list over
     sequences of lists over heads (None for heads not requested) of select_head dicts.
     force_pattern: None, or an int (all heads), or a dict {(seq, head): pattern}."""
@@ -345,7 +416,8 @@ def select(q, k, cu_seqlens, block, gamma, tau, min_budget, scale=None, force_pa
             elif force_pattern is not None:
                 fp = int(force_pattern)
             per_head.append(select_head(q[t0:t1, h], k[t0:t1, h // group], block, gamma, tau,
-                                        min_budget, scale, fp, keep_detail))
+                                        min_budget, scale, fp, keep_detail, max_budget,
+                                        qa_mode))
         out.append(per_head)
     return out
 

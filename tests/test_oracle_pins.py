@@ -254,6 +254,95 @@ def test_query_aware_index_flattening_order():
     np.testing.assert_allclose(sel.scores, a_map[I, J] / a_map[I, J].sum())
 
 
+# ---------------------------------------------------------------- query-wise selection (R11)
+
+@pytest.mark.parametrize("trial", range(12))
+def test_query_aware_rows_brute_force(trial):
+    """Every query block is its own minimal selection over its row of the pooled map:
+    brute force over subsets of each row (normalised by the row's own sum)."""
+    rng = np.random.default_rng(100 + trial)
+    nb = int(rng.integers(1, 7))
+    raw = np.tril(rng.random((nb, nb)) ** 2 + (trial % 3 == 0) * rng.integers(0, 3, (nb, nb)))
+    raw[np.arange(nb), np.arange(nb)] += 1e-3            # no all-zero row
+    gamma = float(rng.choice([0.3, 0.6, 0.9, 0.999]))
+    sels = oracle.query_aware_index_rows(raw, gamma)
+    assert len(sels) == nb
+    for I, sel in enumerate(sels):
+        row = raw[I, :I + 1] / raw[I, :I + 1].sum()
+        size, comb = _brute_min_subset(list(row), gamma)
+        assert sel.k == size, (I, sel.k, size)
+        assert tuple(sorted(sel.selected.tolist())) == comb
+
+
+def test_query_aware_rows_scale_invariance_and_coverage():
+    """Row normalisation: scaling a row of the map does not change its selection, and the
+    mask reaches gamma in every row while flatten selection does not have to."""
+    nb, gamma = 6, 0.8
+    a_map = np.tril(RNG.random((nb, nb)) + 0.05)
+    a_map /= a_map.sum(axis=1, keepdims=True)
+    base = oracle.tiles_from_query_aware_rows(oracle.query_aware_index_rows(a_map, gamma), nb)
+    scaled = a_map * np.arange(1, nb + 1)[:, None] * 7.5
+    again = oracle.tiles_from_query_aware_rows(oracle.query_aware_index_rows(scaled, gamma), nb)
+    np.testing.assert_array_equal(base, again)
+    for I in range(nb):
+        got = a_map[I, base[I]].sum()
+        assert got >= gamma - 1e-12
+        # minimal: dropping the smallest selected block falls below gamma
+        if base[I].sum() > 1:
+            assert got - a_map[I, base[I]].min() < gamma
+    # a peaked row and a flat row: flatten spends the budget on the peaked row first
+    peaked = np.zeros((2, 2))
+    peaked[0, 0] = 1.0
+    peaked[1] = [0.5, 0.5]
+    sel_flat, ids = oracle.query_aware_index(peaked, 0.6)
+    flat_mask = oracle.tiles_from_query_aware(ids[sel_flat.selected], 2)
+    row_mask = oracle.tiles_from_query_aware_rows(oracle.query_aware_index_rows(peaked, 0.6), 2)
+    assert flat_mask.sum() == 2 and not flat_mask[1].all()
+    assert row_mask[1].all() and row_mask[0, 0]
+
+
+# ---------------------------------------------------------------- maximum budget (R12)
+
+def test_max_budget_hand_examples():
+    nb = 6
+    full = np.tril(np.ones((nb, nb), dtype=bool))
+    a_map = np.tril(np.full((nb, nb), 0.01))
+    a_map[4, :5] = [0.05, 0.4, 0.1, 0.3, 0.15]
+    qa = oracle.apply_max_budget(full, oracle.PATTERN_QA, 3, a_map)
+    assert set(np.nonzero(qa[4])[0]) == {0, 1, 4}           # 0, I, then the largest score
+    assert set(np.nonzero(qa[2])[0]) == {0, 1, 2}           # row already within the cap
+    vs = oracle.apply_max_budget(full, oracle.PATTERN_VS, 3)
+    assert set(np.nonzero(vs[5])[0]) == {0, 4, 5}           # nearest to the diagonal
+    assert set(np.nonzero(vs[3])[0]) == {0, 2, 3}
+    two = oracle.apply_max_budget(full, oracle.PATTERN_VS, 2)
+    for I in range(nb):
+        assert set(np.nonzero(two[I])[0]) == ({0, I} if I else {0})
+
+
+@pytest.mark.parametrize("pattern", [0, 1])
+def test_max_budget_properties(pattern):
+    rng = np.random.default_rng(77 + pattern)
+    nb = 20
+    a_map = np.tril(rng.random((nb, nb)))
+    mask = oracle.add_forced_and_min_budget(np.tril(rng.random((nb, nb)) < 0.5), pattern, 3,
+                                            a_map)
+    assert oracle.apply_max_budget(mask, pattern, 0, a_map) is mask       # no cap
+    np.testing.assert_array_equal(oracle.apply_max_budget(mask, pattern, nb, a_map), mask)
+    for M in (2, 4, 7):
+        capped = oracle.apply_max_budget(mask, pattern, M, a_map)
+        assert not np.any(capped & ~mask)                                  # only removes
+        for I in range(nb):
+            row = np.nonzero(capped[I])[0]
+            assert len(row) == min(M, int(mask[I].sum()))
+            assert 0 in row and I in row
+            # what was dropped ranks below everything kept (other than 0 and I)
+            pri = list(oracle.row_priority(I, pattern, a_map))
+            kept = [pri.index(J) for J in row if J not in (0, I)]
+            dropped = [pri.index(J) for J in np.nonzero(mask[I] & ~capped[I])[0]]
+            if kept and dropped:
+                assert max(kept) < min(dropped)
+
+
 # ---------------------------------------------------------------- forced tiles and min budget
 
 def test_forced_and_min_budget():
