@@ -58,6 +58,15 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama128k")
     ap.add_argument("--gamma", type=float, default=None)
+    ap.add_argument("--qa-mode", type=int, default=0,
+                    help="query-aware selection: 0 flattened map (Algorithm 4), 1 per query block")
+    ap.add_argument("--max-budget", type=int, default=0,
+                    help="per-row cap in key blocks (0 = none)")
+    ap.add_argument("--sweep", default=None, metavar="OUT.json",
+                    help="instead of the single measurement, time selection and attention of "
+                         "the Llama-shaped layer from 4k to 128k tokens over a gamma sweep "
+                         "(and dense attention per length), write the table to OUT.json and "
+                         "print a one-line summary")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-sdpa", action="store_true", help="skip the PyTorch SDPA dense timing")
@@ -80,7 +89,7 @@ def time_loop(fn, steps, stream):
     return ev[0].elapsed_time(ev[1]) / steps
 
 
-def cpu_baseline(layer, spec, gamma, n_heads, n_rows):
+def cpu_baseline(layer, spec, gamma, n_heads, n_rows, max_budget=0, qa_mode=0):
     """Oracle on host cores over a bounded sample of the same layer, scaled to ms/layer:
     selection of `n_heads` whole heads, attention on `n_rows` random query-block rows of
     each of them; per-head and per-row means are scaled to all heads and rows."""
@@ -105,7 +114,8 @@ def cpu_baseline(layer, spec, gamma, n_heads, n_rows):
         t0, t1 = int(cu[s]), int(cu[s + 1])
         qs, ks, vs = layer.q[t0:t1, h], layer.k[t0:t1, h // G], layer.v[t0:t1, h // G]
         t = time.perf_counter()
-        r = oracle.select_head(qs, ks, b, gamma, spec.tau, spec.min_budget, scale)
+        r = oracle.select_head(qs, ks, b, gamma, spec.tau, spec.min_budget, scale,
+                               max_budget=max_budget, qa_mode=qa_mode)
         t_sel += time.perf_counter() - t
         nb = r["mask"].shape[0]
         rows = rng.choice(nb, size=min(n_rows, nb), replace=False)
@@ -125,6 +135,83 @@ def cpu_baseline(layer, spec, gamma, n_heads, n_rows):
                        f"{total_rows} rows")}
 
 
+SWEEP_LENGTHS = (4096, 8192, 16384, 32768, 65536, 131072)
+SWEEP_GAMMAS = (0.85, 0.9, 0.95, 0.99)
+
+
+def sweep(args):
+    """Latency breakdown (selection vs attention) and time-vs-gamma of the Llama-shaped
+    layer (32/8 heads, d = 128, tau 0.1, min budget 8) from 4k to 128k tokens; dense
+    attention through the same kernel (every causal block) per length."""
+    import torch
+    import synth
+    import paper_2502_20766_amd as fpx
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    base = synth.SPECS["llama128k"]
+    rows = []
+    for n in SWEEP_LENGTHS:
+        spec = base.with_seqlens((n,), f"llama3-8b-layer-n{n}")
+        layer = synth.make_layer(spec)
+        q = torch.from_numpy(layer.q).to(torch.bfloat16).to(dev)
+        k = torch.from_numpy(layer.k).to(torch.bfloat16).to(dev)
+        v = torch.from_numpy(layer.v).to(torch.bfloat16).to(dev)
+        cu = layer.cu_seqlens
+        shape = fpx.Shape(cu, spec.hq, spec.hkv, spec.d, spec.block)
+        ws_att = torch.empty(max(fpx.attn_workspace_size(shape), 1), dtype=torch.uint8,
+                             device=dev)
+        o = torch.empty_like(q)
+        nb = -(-n // spec.block)
+        causal_tiles = spec.hq * nb * (nb + 1) // 2
+        reps = max(3, min(20, int(2e5 // n)))
+        idx_d = fpx.select(q, k, cu, 1.0, spec.tau, spec.min_budget)
+        fpx.sparse_attn(q, k, v, idx_d, out=o, workspace=ws_att)
+        ms_dense = time_loop(lambda: fpx.sparse_attn(q, k, v, idx_d, out=o, workspace=ws_att),
+                             max(2, reps // 2), stream)
+        del idx_d
+        for gamma in SWEEP_GAMMAS:
+            p = fpx.params(gamma, spec.tau, spec.min_budget, qa_mode=args.qa_mode,
+                           max_budget=args.max_budget)
+            ws_sel = torch.empty(max(fpx.select_workspace_size(shape, p), 1), dtype=torch.uint8,
+                                 device=dev)
+            idx = fpx.empty_indices(shape, dev)
+
+            def sel():
+                fpx.select(q, k, cu, gamma, spec.tau, spec.min_budget, out=idx, workspace=ws_sel,
+                           qa_mode=args.qa_mode, max_budget=args.max_budget)
+
+            def att():
+                fpx.sparse_attn(q, k, v, idx, out=o, workspace=ws_att)
+            sel()
+            att()
+            torch.cuda.synchronize()
+            ms_sel = time_loop(sel, reps, stream)
+            ms_att = time_loop(att, reps, stream)
+            tiles = int(idx.kb_cnt.sum().item())
+            row = {"n": n, "gamma": gamma, "select_ms": round(ms_sel, 4),
+                   "attn_ms": round(ms_att, 4), "layer_ms": round(ms_sel + ms_att, 4),
+                   "select_share": round(ms_sel / (ms_sel + ms_att), 4),
+                   "density": round(tiles / causal_tiles, 5),
+                   "attn_tflops_on_computed_blocks": round(
+                       4 * spec.block ** 2 * spec.d * tiles / (ms_att * 1e-3) / 1e12, 2),
+                   "dense_ms": round(ms_dense, 4),
+                   "speedup_vs_dense": round(ms_dense / (ms_sel + ms_att), 3)}
+            rows.append(row)
+            log(f"[sweep] n={n:6d} gamma={gamma:.2f} select {ms_sel:8.3f} attn {ms_att:8.3f} "
+                f"dense {ms_dense:8.3f} ms density {row['density']:.4f}")
+            del idx, ws_sel
+        del q, k, v, o, ws_att, layer
+        torch.cuda.empty_cache()
+    table = {"workload": "llama3-8b-layer, 32/8 heads, d 128, tau 0.1, min budget 8 blocks",
+             "qa_mode": args.qa_mode, "max_budget_blocks": args.max_budget,
+             "data": "synthetic (seeded vertical-slash / clustered heads, bf16)", "rows": rows}
+    with open(args.sweep, "w") as f:
+        json.dump(table, f, indent=1)
+    last = [r for r in rows if r["n"] == SWEEP_LENGTHS[-1]]
+    print(json.dumps({"sweep": args.sweep, "points": len(rows),
+                      "at_128k": {str(r["gamma"]): r["layer_ms"] for r in last}}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -132,6 +219,9 @@ def main():
                                    "needs no cross-GPU communication and multi-GPU runs are "
                                    "not part of it; run with --gpus 1"}))
         sys.exit(2)
+    if args.sweep:
+        sweep(args)
+        return
     import torch
     import synth
     import paper_2502_20766_amd as fpx
@@ -158,7 +248,8 @@ def main():
     cu = layer.cu_seqlens
     stream = torch.cuda.current_stream()
     shape = fpx.Shape(cu, spec.hq, spec.hkv, spec.d, spec.block)
-    p = fpx.params(gamma, spec.tau, spec.min_budget)
+    sel_kw = dict(max_budget=args.max_budget, qa_mode=args.qa_mode)
+    p = fpx.params(gamma, spec.tau, spec.min_budget, **sel_kw)
     ws_sel = torch.empty(max(fpx.select_workspace_size(shape, p), 1), dtype=torch.uint8,
                          device=dev)
     ws_att = torch.empty(max(fpx.attn_workspace_size(shape), 1), dtype=torch.uint8, device=dev)
@@ -166,7 +257,8 @@ def main():
     o = torch.empty_like(q)
 
     def do_select():
-        fpx.select(q, k, cu, gamma, spec.tau, spec.min_budget, out=idx, workspace=ws_sel)
+        fpx.select(q, k, cu, gamma, spec.tau, spec.min_budget, out=idx, workspace=ws_sel,
+                   **sel_kw)
 
     def do_attn():
         fpx.sparse_attn(q, k, v, idx, out=o, workspace=ws_att)
@@ -241,7 +333,8 @@ def main():
         "data": "synthetic (seeded vertical-slash / clustered heads, bf16)",
         "config": {"workload": spec.name, "seqlens": list(map(int, seqlens)), "q_heads": spec.hq,
                    "kv_heads": spec.hkv, "head_dim": spec.d, "block": spec.block,
-                   "gamma": gamma, "tau": spec.tau, "min_budget_blocks": spec.min_budget},
+                   "gamma": gamma, "tau": spec.tau, "min_budget_blocks": spec.min_budget,
+                   "max_budget_blocks": args.max_budget, "qa_mode": args.qa_mode},
         "select_ms": round(ms_select, 4),
         "attn_ms": round(ms_attn, 4),
         "effective_tflops": round(f_dense / (ms_step * 1e-3) / 1e12, 2),
@@ -262,7 +355,7 @@ def main():
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle, bounded sample)")
         result["cpu_baseline"] = cpu_baseline(layer, spec, gamma, args.cpu_sample_heads,
-                                              args.cpu_sample_rows)
+                                              args.cpu_sample_rows, **sel_kw)
     print(json.dumps(result), flush=True)
 
 

@@ -71,6 +71,14 @@ typedef struct fp_params {
                               /* blocks; 0..FP_MAX_MIN_BUDGET (paper: 1024 tokens = 8)*/
   float softmax_scale;        /* 0 => 1/sqrt(head_dim)                                */
   int32_t force_pattern;      /* -1 decide by JS; 0 force query-aware; 1 force VS     */
+  int32_t max_budget_blocks;  /* 0: no cap; M >= 2 (and >= min_budget_blocks): every  */
+                              /* row keeps <= M key blocks -- 0 and I, then the rest  */
+                              /* in top-up order (appendix "maximum budget limit")    */
+  int32_t qa_mode;            /* query-aware selection: 0 over the flattened pooled   */
+                              /* map (Algorithm 4); 1 per query block, each row of    */
+                              /* the map reaching gamma (appendix "flatten ablation") */
+  int32_t vs_granularity;     /* vertical-slash lines: 0 token lines (Algorithm 3);   */
+                              /* 1 block-pooled lines (reserved: FP_ERR_UNSUPPORTED)  */
 } fp_params;
 
 /* Outputs of fp_select (caller-allocated device buffers; sizes from fp_indices_size).
@@ -84,8 +92,9 @@ typedef struct fp_params {
  *   pattern: uint8 [batch * Hq], FP_PATTERN_* per (s, h) at s*Hq + h.
  *   js     : float [batch * Hq], D_JS per (s, h) (negative when not computed).
  *   units  : int32 [batch * Hq * 2], per (s, h): {K, 0} for query-aware heads (units
- *            selected by Algorithm 4), {K_v, K_s} for vertical-slash heads, {all, 0}
- *            when dense. Diagnostics only. */
+ *            selected by Algorithm 4; with qa_mode 1 the sum over query blocks of
+ *            their K), {K_v, K_s} for vertical-slash heads, {all, 0} when dense.
+ *            Diagnostics only. */
 typedef struct fp_indices {
   int32_t *kb_idx;
   int32_t *kb_cnt;

@@ -37,7 +37,8 @@ class FpShape(ctypes.Structure):
 class FpParams(ctypes.Structure):
     _fields_ = [("gamma", ctypes.c_float), ("tau", ctypes.c_float),
                 ("min_budget_blocks", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
-                ("force_pattern", ctypes.c_int32)]
+                ("force_pattern", ctypes.c_int32), ("max_budget_blocks", ctypes.c_int32),
+                ("qa_mode", ctypes.c_int32), ("vs_granularity", ctypes.c_int32)]
 
 
 class FpIndices(ctypes.Structure):
@@ -103,9 +104,10 @@ class Shape:
         return -(-self.seqlens // self.block)
 
 
-def params(gamma, tau, min_budget=8, softmax_scale=0.0, force_pattern=-1) -> FpParams:
+def params(gamma, tau, min_budget=8, softmax_scale=0.0, force_pattern=-1, max_budget=0,
+           qa_mode=0, vs_granularity=0) -> FpParams:
     return FpParams(float(gamma), float(tau), int(min_budget), float(softmax_scale),
-                    int(force_pattern))
+                    int(force_pattern), int(max_budget), int(qa_mode), int(vs_granularity))
 
 
 def indices_size(shape: Shape):
@@ -174,7 +176,8 @@ def empty_indices(shape: Shape, device):
 
 
 def select(q, k, cu_seqlens, gamma, tau, min_budget=8, block=128, softmax_scale=0.0,
-           force_pattern=-1, out: Indices | None = None, workspace=None, stream=None) -> Indices:
+           force_pattern=-1, out: Indices | None = None, workspace=None, stream=None,
+           max_budget=0, qa_mode=0, vs_granularity=0) -> Indices:
     """Pattern search + index selection (Algorithms 2-4) for a packed layer.
 
     q: [T, Hq, d] bf16 CUDA, k: [T, Hkv, d] bf16 CUDA, cu_seqlens: host ints [B+1]."""
@@ -182,7 +185,8 @@ def select(q, k, cu_seqlens, gamma, tau, min_budget=8, block=128, softmax_scale=
     _check_tensor(q, "q", 3)
     _check_tensor(k, "k", 3)
     shape = Shape(cu_seqlens, q.shape[1], k.shape[1], q.shape[2], block)
-    p = params(gamma, tau, min_budget, softmax_scale, force_pattern)
+    p = params(gamma, tau, min_budget, softmax_scale, force_pattern, max_budget, qa_mode,
+               vs_granularity)
     ws_bytes = select_workspace_size(shape, p)
     if workspace is None:
         workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)

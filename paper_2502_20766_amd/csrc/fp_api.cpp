@@ -79,6 +79,12 @@ fp_status check_params(const fp_shape *sh, const fp_params *p) {
   if (p->softmax_scale < 0.f || isnan(p->softmax_scale) || isinf(p->softmax_scale))
     return FP_ERR_INVALID_ARG;
   if (p->force_pattern < -1 || p->force_pattern > 1) return FP_ERR_INVALID_ARG;
+  if (p->max_budget_blocks < 0 || p->max_budget_blocks == 1) return FP_ERR_INVALID_ARG;
+  if (p->max_budget_blocks > 0 && p->max_budget_blocks < p->min_budget_blocks)
+    return FP_ERR_INVALID_ARG;
+  if (p->qa_mode < 0 || p->qa_mode > 1) return FP_ERR_INVALID_ARG;
+  if (p->vs_granularity < 0 || p->vs_granularity > 1) return FP_ERR_INVALID_ARG;
+  if (p->vs_granularity == 1) return FP_ERR_UNSUPPORTED;
   (void)sh;
   return FP_OK;
 }
@@ -203,6 +209,8 @@ fp_status fp_select(const fp_shape *shape, const void *q, const void *k, const f
   a.tau = params->tau;
   a.min_budget = params->min_budget_blocks;
   a.force_pattern = params->force_pattern;
+  a.max_budget = params->max_budget_blocks;
+  a.qa_mode = params->qa_mode;
   a.kb_idx = out->kb_idx;
   a.kb_cnt = out->kb_cnt;
   a.pattern = out->pattern;

@@ -36,6 +36,8 @@ struct SelectArgs {
   float gamma, tau;
   int32_t min_budget;
   int32_t force_pattern;
+  int32_t max_budget;      // 0 = no cap
+  int32_t qa_mode;         // 0 flattened map (Algorithm 4), 1 per query block
   // workspace
   float2 *chunk_stats;     // [ch_total][Hq][block] (max, sum) in log2 units
   float2 *row_stats;       // [n_seq][Hq][block]
@@ -90,5 +92,6 @@ struct AttnArgs {
 hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t s);
 hipError_t launch_select_pipeline(const SelectArgs &a, hipStream_t s);
 hipError_t launch_dense_lists(const SelectArgs &a, hipStream_t s);
+hipError_t launch_qa_rows(const SelectArgs &a, hipStream_t s);
 
 }  // namespace fp

@@ -18,7 +18,11 @@
 // (t < rows of the query block), and the diagonal Delta+1 when t > 0.  Query-aware heads
 // mark their selected (I, J) units.  Every row then keeps key blocks 0 and I and is
 // topped up to min(m, I+1) blocks (query-aware: highest pooled score first, then lowest
-// J; vertical-slash: nearest the diagonal first) -- the guards of Section 4.1.
+// J; vertical-slash: nearest the diagonal first) -- the guards of Section 4.1.  With a
+// maximum budget M, rows above M blocks keep 0, I and their other blocks in that same
+// order (appendix "maximum budget limit").  Query-aware heads may instead select per query
+// block (appendix "flatten ablation"); those rows, and capped query-aware rows, are
+// finished by qa_rows.
 #include "fp_internal.h"
 
 namespace fp {
@@ -56,7 +60,7 @@ __device__ __forceinline__ Problem problem_of(const SelectArgs &a, int p) {
     pr.scores = (kind == 0 ? a.a_v : a.a_s) + (int64_t)h * a.total_tokens + tok0;
     pr.n = n;
     pr.active = true;
-  } else if (pat == FP_PATTERN_QUERY_AWARE && kind == 0) {
+  } else if (pat == FP_PATTERN_QUERY_AWARE && kind == 0 && a.qa_mode == 0) {
     const int nb = a.st.nb_off[s + 1] - a.st.nb_off[s];
     pr.scores = a.flat + (int64_t)h * a.tri_total + a.st.tri_off[s];
     pr.n = nb * (nb + 1) / 2;
@@ -298,9 +302,11 @@ __global__ __launch_bounds__(1024) void convert_tiles(SelectArgs a) {
     __syncthreads();
   }
   if (tid == 0) {
-    a.units[(s * a.hq + h) * 2 + 0] = S0.k;
+    // per-query-block selection accumulates its K over the rows (qa_rows, launched next)
+    a.units[(s * a.hq + h) * 2 + 0] = (!vs && a.qa_mode == 1) ? 0 : S0.k;
     a.units[(s * a.hq + h) * 2 + 1] = vs ? S1.k : 0;
   }
+  if (!vs && (a.qa_mode == 1 || a.max_budget > 0)) return;   // rows written by qa_rows
 
   const int m = a.min_budget;
   for (int I = w; I < nb; I += 16) {
@@ -364,21 +370,183 @@ __global__ __launch_bounds__(1024) void convert_tiles(SelectArgs a) {
         }
       }
     }
+    auto kept = [&](int J) -> bool {
+      bool f = sel(J) || (J >= jmin && J < I);
+      for (int q = 0; q < n_added; ++q) f |= (added[w][q] == J);
+      return f;
+    };
+    // maximum budget (vertical-slash rows; query-aware rows are capped in qa_rows): keep
+    // blocks 0 and I and the nearest-to-diagonal others, i.e. every kept J >= jcap
+    int jcap = 0;
+    if (vs && a.max_budget > 0 && I > 0) {
+      int total = 0;
+      for (int J0 = 0; J0 <= I; J0 += 64) {
+        const int J = J0 + lane;
+        total += __popcll(__ballot(J <= I && kept(J)));
+      }
+      if (total > a.max_budget) {
+        int need = a.max_budget - 2;               // others to keep, nearest I first
+        jcap = I;                                    // need == 0: no other block
+        for (int top = I - 1; top >= 1 && need > 0; top -= 64) {
+          const int J = top - lane;
+          const bool f = J >= 1 && kept(J);
+          const unsigned long long bal = __ballot(f);
+          const int c = __popcll(bal);
+          if (c >= need) {
+            const int rank = __popcll(bal & __lanemask_lt());
+            const unsigned long long pick = __ballot(f && rank == need - 1);
+            jcap = top - (__ffsll((long long)pick) - 1);
+            need = 0;
+          } else {
+            need -= c;
+          }
+        }
+      }
+    }
     int32_t *out = a.kb_idx + (int64_t)h * a.tri_total + a.st.tri_off[s] + tri_row;
     int running = 0;
     for (int J0 = 0; J0 <= I; J0 += 64) {
       const int J = J0 + lane;
-      bool f = false;
-      if (J <= I) {
-        f = sel(J) || (J >= jmin && J < I);
-        for (int q = 0; q < n_added; ++q) f |= (added[w][q] == J);
-      }
+      const bool f = J <= I && kept(J) && (J == 0 || J == I || J >= jcap);
       const unsigned long long bal = __ballot(f);
       if (f) out[running + __popcll(bal & __lanemask_lt())] = J;
       running += __popcll(bal);
     }
     if (lane == 0) a.kb_cnt[(int64_t)h * a.nb_total + a.st.nb_off[s] + I] = running;
   }
+}
+
+// Query-aware rows when the selection is per query block (qa_mode 1) or rows are capped
+// (max_budget > 0).  One workgroup per (query head, query block I): the row's pooled scores
+// A_bar[I, J], J <= I, are sorted in LDS by (score desc, J asc).  The gamma-selected units
+// of the row are then a prefix of that order in both modes (flattened: the head's radix
+// threshold; per query block: the shortest prefix whose exact fixed-point mass reaches
+// ceil(gamma * row total)).  Blocks 0 and I are always kept; the other blocks are taken
+// along the same order: the selected prefix, raised to min(m, I+1) blocks in total by the
+// top-up and lowered to max_budget by the cap.
+constexpr int kRowThreads = 256;
+
+__global__ __launch_bounds__(kRowThreads) void qa_rows(SelectArgs a) {
+  __shared__ unsigned long long key[kMaxNb];       // (~score bits) << 32 | J
+  __shared__ unsigned long long pref[kRowThreads];
+  __shared__ uint8_t keep[kMaxNb];
+  __shared__ int s_pos0, s_posI, s_kcut;
+  __shared__ uint32_t wcnt[kRowThreads / 64];
+  const int h = blockIdx.y;
+  const int row = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  int s = 0;
+  while (s + 1 < a.st.n_seq && a.st.nb_off[s + 1] <= row) ++s;
+  if (a.pattern[s * a.hq + h] != FP_PATTERN_QUERY_AWARE) return;
+  const int I = row - a.st.nb_off[s];
+  const int len = I + 1;
+  const int64_t tri_row = (int64_t)I * (I + 1) / 2;
+  const float *x = a.flat + (int64_t)h * a.tri_total + a.st.tri_off[s] + tri_row;
+  int np = 1;
+  while (np < len) np <<= 1;
+  for (int i = tid; i < np; i += kRowThreads) {
+    key[i] = i < len ? ((unsigned long long)(~__float_as_uint(x[i])) << 32) | (uint32_t)i
+                     : ~0ull;
+    if (i < len) keep[i] = 0;
+  }
+  if (tid == 0) s_kcut = len;
+  __syncthreads();
+  for (int size = 2; size <= np; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = tid; i < np; i += kRowThreads) {
+        const int j = i ^ stride;
+        if (j > i) {
+          const bool up = (i & size) == 0;
+          const unsigned long long u = key[i], v = key[j];
+          if (up ? (u > v) : (u < v)) {
+            key[i] = v;
+            key[j] = u;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // thread t owns the sorted positions [t*per, (t+1)*per)
+  const int per = (len + kRowThreads - 1) / kRowThreads;
+  const int p_lo = min(tid * per, len), p_hi = min(p_lo + per, len);
+  auto score_at = [&](int p) { return __uint_as_float(~(uint32_t)(key[p] >> 32)); };
+  auto id_at = [&](int p) { return (int)(key[p] & 0xFFFFFFFFu); };
+  int K = len;                                       // gamma-selected units of the row
+  if (a.qa_mode == 1) {
+    unsigned long long mine = 0;
+    for (int p = p_lo; p < p_hi; ++p) mine += to_fx(score_at(p));
+    pref[tid] = mine;
+    __syncthreads();
+    for (int off = 1; off < kRowThreads; off <<= 1) {      // inclusive scan (integers)
+      const unsigned long long v = tid >= off ? pref[tid - off] : 0ull;
+      __syncthreads();
+      pref[tid] += v;
+      __syncthreads();
+    }
+    const unsigned long long total = pref[kRowThreads - 1];
+    unsigned long long thr = (unsigned long long)ceil((double)a.gamma * (double)total);
+    if (thr < 1ull) thr = 1ull;
+    if (total > 0ull && thr <= total) {
+      unsigned long long run = pref[tid] - mine;
+      for (int p = p_lo; p < p_hi; ++p) {
+        run += to_fx(score_at(p));
+        if (run >= thr) {
+          atomicMin(&s_kcut, p + 1);
+          break;
+        }
+      }
+    }
+    __syncthreads();
+    K = s_kcut;
+    if (tid == 0) atomicAdd(&a.units[(s * a.hq + h) * 2], K);
+  } else {
+    const SelState S0 = a.sel[(s * a.hq + h) * 2];
+    int c = 0;
+    for (int p = p_lo; p < p_hi; ++p) c += is_selected(S0, score_at(p), (int)(tri_row + id_at(p)));
+    c = (int)__reduce_add_sync(~0ull, (unsigned)c);
+    if (lane == 0) wcnt[w] = (uint32_t)c;
+    __syncthreads();
+    K = 0;
+    for (int q = 0; q < kRowThreads / 64; ++q) K += (int)wcnt[q];
+  }
+  // positions of the forced blocks 0 and I in the order
+  for (int p = p_lo; p < p_hi; ++p) {
+    const int J = id_at(p);
+    if (J == 0) s_pos0 = p;
+    if (J == I) s_posI = p;
+  }
+  __syncthreads();
+  const int pos0 = s_pos0, posI = s_posI;
+  const int f = I == 0 ? 1 : 2;                       // forced blocks
+  const int in_f = (pos0 < K) + (I > 0 && posI < K);
+  int k_final = K - in_f;                             // other blocks, along the order
+  k_final = max(k_final, min(a.min_budget, len) - f);
+  if (a.max_budget > 0) k_final = min(k_final, a.max_budget - f);
+  for (int p = p_lo; p < p_hi; ++p) {
+    const int J = id_at(p);
+    const int rank = p - (pos0 < p) - (I > 0 && posI < p);   // position among the others
+    if (J == 0 || J == I || rank < k_final) keep[J] = 1;
+  }
+  __syncthreads();
+  int32_t *out = a.kb_idx + (int64_t)h * a.tri_total + a.st.tri_off[s] + tri_row;
+  int running = 0;
+  for (int J0 = 0; J0 < len; J0 += kRowThreads) {
+    const int J = J0 + tid;
+    const bool fl = J < len && keep[J];
+    const unsigned long long bal = __ballot(fl);
+    if (lane == 0) wcnt[w] = (uint32_t)__popcll(bal);
+    __syncthreads();
+    int before = 0, chunk = 0;
+    for (int q = 0; q < kRowThreads / 64; ++q) {
+      if (q < w) before += (int)wcnt[q];
+      chunk += (int)wcnt[q];
+    }
+    if (fl) out[running + before + __popcll(bal & __lanemask_lt())] = J;
+    running += chunk;
+    __syncthreads();
+  }
+  if (tid == 0) a.kb_cnt[(int64_t)h * a.nb_total + row] = running;
 }
 
 // gamma >= 1: every causal key block, no search (full attention).
@@ -403,6 +571,11 @@ __global__ __launch_bounds__(256) void dense_lists(SelectArgs a) {
 }
 
 }  // namespace
+
+hipError_t launch_qa_rows(const SelectArgs &a, hipStream_t stream) {
+  hipLaunchKernelGGL(qa_rows, dim3(a.nb_total, a.hq), dim3(kRowThreads), 0, stream, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_dense_lists(const SelectArgs &a, hipStream_t stream) {
   hipLaunchKernelGGL(dense_lists, dim3((a.nb_total + 3) / 4, a.hq), dim3(256), 0, stream, a);
@@ -432,6 +605,10 @@ hipError_t launch_select_pipeline(const SelectArgs &a, hipStream_t stream) {
   hipLaunchKernelGGL(sel_scan<2>, dim3(problems), dim3(256), 0, stream, a);
   hipLaunchKernelGGL(sel_tie, dim3(problems), dim3(1024), 0, stream, a);
   hipLaunchKernelGGL(convert_tiles, dim3(a.st.n_seq * a.hq), dim3(1024), 0, stream, a);
+  if (a.qa_mode == 1 || a.max_budget > 0) {
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return launch_qa_rows(a, stream);
+  }
   return hipGetLastError();
 }
 

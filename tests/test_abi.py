@@ -91,6 +91,15 @@ def test_validate_shape_errors(lib, kw, status):
     (dict(gamma=0.9, tau=0.1, min_budget=65), fpx.FP_ERR_UNSUPPORTED),
     (dict(gamma=0.9, tau=0.1, softmax_scale=-1.0), fpx.FP_ERR_INVALID_ARG),
     (dict(gamma=0.9, tau=0.1, force_pattern=2), fpx.FP_ERR_INVALID_ARG),
+    (dict(gamma=0.9, tau=0.1, max_budget=-1), fpx.FP_ERR_INVALID_ARG),
+    (dict(gamma=0.9, tau=0.1, max_budget=1), fpx.FP_ERR_INVALID_ARG),     # cannot hold 0, I
+    (dict(gamma=0.9, tau=0.1, min_budget=8, max_budget=4), fpx.FP_ERR_INVALID_ARG),
+    (dict(gamma=0.9, tau=0.1, min_budget=8, max_budget=8), fpx.FP_OK),
+    (dict(gamma=0.9, tau=0.1, min_budget=2, max_budget=2), fpx.FP_OK),
+    (dict(gamma=0.9, tau=0.1, qa_mode=2), fpx.FP_ERR_INVALID_ARG),
+    (dict(gamma=0.9, tau=0.1, qa_mode=1), fpx.FP_OK),
+    (dict(gamma=0.9, tau=0.1, vs_granularity=-1), fpx.FP_ERR_INVALID_ARG),
+    (dict(gamma=0.9, tau=0.1, vs_granularity=1), fpx.FP_ERR_UNSUPPORTED),
     (dict(gamma=0.9, tau=0.1), fpx.FP_OK),
     (dict(gamma=1.0, tau=0.0, min_budget=64, force_pattern=1), fpx.FP_OK),
 ])
