@@ -426,10 +426,12 @@ __global__ __launch_bounds__(1024) void convert_tiles(SelectArgs a) {
 // top-up and lowered to max_budget by the cap.
 constexpr int kRowThreads = 256;
 
-__global__ __launch_bounds__(kRowThreads) void qa_rows(SelectArgs a) {
-  __shared__ unsigned long long key[kMaxNb];       // (~score bits) << 32 | J
+__global__ __launch_bounds__(kRowThreads) void qa_rows(SelectArgs a, int np_max) {
+  // dynamic LDS sized by the longest row: key[np_max] then keep[np_max]
+  extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
+  unsigned long long *key = reinterpret_cast<unsigned long long *>(dyn);  // (~bits) << 32 | J
+  uint8_t *keep = dyn + (size_t)np_max * sizeof(unsigned long long);
   __shared__ unsigned long long pref[kRowThreads];
-  __shared__ uint8_t keep[kMaxNb];
   __shared__ int s_pos0, s_posI, s_kcut;
   __shared__ uint32_t wcnt[kRowThreads / 64];
   const int h = blockIdx.y;
@@ -573,7 +575,16 @@ __global__ __launch_bounds__(256) void dense_lists(SelectArgs a) {
 }  // namespace
 
 hipError_t launch_qa_rows(const SelectArgs &a, hipStream_t stream) {
-  hipLaunchKernelGGL(qa_rows, dim3(a.nb_total, a.hq), dim3(kRowThreads), 0, stream, a);
+  int np_max = 1;
+  while (np_max < a.st.max_nb) np_max <<= 1;
+  const size_t dyn = (size_t)np_max * (sizeof(unsigned long long) + 1);
+  if (dyn > 65536) {          // rows above 7281 blocks: allow the larger LDS allocation
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(qa_rows),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             (int)dyn);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(qa_rows, dim3(a.nb_total, a.hq), dim3(kRowThreads), dyn, stream, a, np_max);
   return hipGetLastError();
 }
 
