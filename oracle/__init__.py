@@ -23,6 +23,8 @@ from .flexprefill import (  # noqa: F401
     sparse_pattern_search,
     cumulative_select,
     vertical_slash_index,
+    vertical_slash_index_pooled,
+    lines_of_blocks,
     query_aware_block_attention,
     query_aware_index,
     query_aware_index_rows,

@@ -38,6 +38,11 @@ Readings taken where the paper is silent (each is also listed in the design note
       keeps blocks 0 and I and then its other blocks in the order R8 uses to add them
       (pooled score for query-aware heads, nearest to the diagonal for vertical-slash
       heads).  M = 0 means no cap.
+  R13 Block-pooled vertical-slash lines (the alternative to Algorithm 3's token lines):
+      a vertical unit is a key block J scored by the sum of a_v over its keys, a slash
+      unit is an offset block [D*b, D*b + b) scored by the sum of a_s over its offsets;
+      each family is selected by the rule of R6, and selecting a unit selects all of its
+      lines, which then mark tiles as in R7.
 """
 from __future__ import annotations
 
@@ -203,6 +208,25 @@ def vertical_slash_index(a_hat: np.ndarray, rows: np.ndarray, gamma: float):
     return cumulative_select(a_v, gamma), cumulative_select(a_s, gamma), a_v, a_s
 
 
+def vertical_slash_index_pooled(a_hat: np.ndarray, rows: np.ndarray, gamma: float,
+                                block: int):
+    """Block-pooled variant of Algorithm 3 (R13): a_v and a_s summed over blocks of `block`
+    key positions / offsets, each selected by cumulative mass.  Returns the two selections
+    (unit ids = block indices) and the pooled scores."""
+    a_v, a_s = vertical_slash_scores(a_hat, rows)
+    n = a_v.shape[0]
+    nb = -(-n // block)
+    pv = np.array([a_v[J * block:(J + 1) * block].sum() for J in range(nb)])
+    ps = np.array([a_s[D * block:(D + 1) * block].sum() for D in range(nb)])
+    return cumulative_select(pv, gamma), cumulative_select(ps, gamma), pv, ps
+
+
+def lines_of_blocks(units, n: int, block: int) -> np.ndarray:
+    """Every line (key position or offset) of the given blocks of lines (R13)."""
+    out = [np.arange(u * block, min((u + 1) * block, n)) for u in np.asarray(units, dtype=int)]
+    return np.concatenate(out) if out else np.zeros(0, dtype=np.int64)
+
+
 def tiles_from_vertical_slash(verticals, slashes, n: int, block: int) -> np.ndarray:
     """Extend the selected lines to the whole attention matrix (Section 3, vertical-slash
     head, third item) and mark each block_size x block_size tile the lines meet (R7).
@@ -351,11 +375,12 @@ def apply_max_budget(mask: np.ndarray, pattern: int, max_budget: int,
 # ------------------------------------------------------------------ Algorithm 1 selection part
 
 def select_head(q_seq, k_seq, block, gamma, tau, min_budget, scale, force_pattern=-1,
-                keep_detail=False, max_budget=0, qa_mode=0):
+                keep_detail=False, max_budget=0, qa_mode=0, vs_granularity=0):
     """Pattern search and index selection for one head of one sequence (Algorithm 1 up to
     the final attention).  qa_mode 0 selects query-aware units over the flattened map
-    (Algorithm 4), 1 per query block (R11); max_budget caps the rows (R12).  Returns a
-    dict with pattern, d_js, tile mask and counts."""
+    (Algorithm 4), 1 per query block (R11); max_budget caps the rows (R12);
+    vs_granularity 0 selects token lines (Algorithm 3), 1 block-pooled lines (R13).
+    Returns a dict with pattern, d_js, tile mask and counts."""
     n = q_seq.shape[0]
     nb = -(-n // block)
     if gamma >= 1.0:                                          # R9
@@ -384,8 +409,14 @@ def select_head(q_seq, k_seq, block, gamma, tau, min_budget, scale, force_patter
         mask = add_forced_and_min_budget(mask, PATTERN_QA, min_budget, a_map)
         mask = apply_max_budget(mask, PATTERN_QA, max_budget, a_map)
     else:
-        sel_v, sel_s, a_v, a_s = vertical_slash_index(a_full, rows, gamma)
-        mask = tiles_from_vertical_slash(sel_v.selected, sel_s.selected, n, block)
+        if vs_granularity == 1:
+            sel_v, sel_s, a_v, a_s = vertical_slash_index_pooled(a_full, rows, gamma, block)
+            mask = tiles_from_vertical_slash(lines_of_blocks(sel_v.selected, n, block),
+                                             lines_of_blocks(sel_s.selected, n, block), n,
+                                             block)
+        else:
+            sel_v, sel_s, a_v, a_s = vertical_slash_index(a_full, rows, gamma)
+            mask = tiles_from_vertical_slash(sel_v.selected, sel_s.selected, n, block)
         mask = add_forced_and_min_budget(mask, PATTERN_VS, min_budget)
         mask = apply_max_budget(mask, PATTERN_VS, max_budget)
         units = (sel_v.k, sel_s.k)
@@ -395,7 +426,7 @@ def select_head(q_seq, k_seq, block, gamma, tau, min_budget, scale, force_patter
 
 
 def select(q, k, cu_seqlens, block, gamma, tau, min_budget, scale=None, force_pattern=None,
-           heads=None, keep_detail=False, max_budget=0, qa_mode=0):
+           heads=None, keep_detail=False, max_budget=0, qa_mode=0, vs_granularity=0):
     """Selection for a packed layer.  q: [T, Hq, d], k: [T, Hkv, d].  Returns a list over
     sequences of lists over heads (None for heads not requested) of select_head dicts.
     force_pattern: None, or an int (all heads), or a dict {(seq, head): pattern}."""
@@ -417,7 +448,7 @@ def select(q, k, cu_seqlens, block, gamma, tau, min_budget, scale=None, force_pa
                 fp = int(force_pattern)
             per_head.append(select_head(q[t0:t1, h], k[t0:t1, h // group], block, gamma, tau,
                                         min_budget, scale, fp, keep_detail, max_budget,
-                                        qa_mode))
+                                        qa_mode, vs_granularity))
         out.append(per_head)
     return out
 

@@ -343,6 +343,45 @@ def test_max_budget_properties(pattern):
                 assert max(kept) < min(dropped)
 
 
+# ---------------------------------------------------------------- block-pooled lines (R13)
+
+@pytest.mark.parametrize("n,block", [(1, 8), (7, 8), (8, 8), (9, 8), (47, 8), (130, 32)])
+def test_pooled_vertical_slash_scores_and_tiles(n, block):
+    """Pooled scores are block sums of the token-line scores (each family sums to 1), and
+    the tiles of the selected blocks equal the token-line tiles of all their lines,
+    checked against a brute-force token mask."""
+    rng = np.random.default_rng(n * 31 + block)
+    q = rng.standard_normal((n, 4))
+    k = rng.standard_normal((n, 4))
+    q_hat, rows = oracle.representative_queries(q, block)
+    a_full = oracle.representative_attention(q_hat, rows, k, 0.5)
+    a_v, a_s = oracle.vertical_slash_scores(a_full, rows)
+    for gamma in (0.3, 0.7, 0.95):
+        sv, ss, pv, ps = oracle.vertical_slash_index_pooled(a_full, rows, gamma, block)
+        nb = -(-n // block)
+        assert pv.shape == (nb,) and ps.shape == (nb,)
+        assert pv.sum() == pytest.approx(1.0, abs=1e-12)
+        assert ps.sum() == pytest.approx(1.0, abs=1e-12)
+        for J in range(nb):
+            assert pv[J] == pytest.approx(a_v[J * block:(J + 1) * block].sum(), abs=1e-15)
+        vl = oracle.lines_of_blocks(sv.selected, n, block)
+        sl = oracle.lines_of_blocks(ss.selected, n, block)
+        assert len(vl) == sum(min((J + 1) * block, n) - J * block for J in sv.selected)
+        got = oracle.tiles_from_vertical_slash(vl, sl, n, block)
+        # brute force: token mask of the lines, tiles that hold a masked causal position
+        tok = np.zeros((n, n), dtype=bool)
+        for j in vl:
+            tok[j:, j] = True
+        for o in sl:
+            i = np.arange(o, n)
+            tok[i, i - o] = True
+        want = np.zeros((nb, nb), dtype=bool)
+        for I in range(nb):
+            for J in range(I + 1):
+                want[I, J] = tok[I * block:(I + 1) * block, J * block:(J + 1) * block].any()
+        np.testing.assert_array_equal(got, want)
+
+
 # ---------------------------------------------------------------- forced tiles and min budget
 
 def test_forced_and_min_budget():
