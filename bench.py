@@ -62,6 +62,8 @@ def parse():
                     help="query-aware selection: 0 flattened map (Algorithm 4), 1 per query block")
     ap.add_argument("--max-budget", type=int, default=0,
                     help="per-row cap in key blocks (0 = none)")
+    ap.add_argument("--vs-granularity", type=int, default=0,
+                    help="vertical-slash lines: 0 token lines (Algorithm 3), 1 block-pooled")
     ap.add_argument("--sweep", default=None, metavar="OUT.json",
                     help="instead of the single measurement, time selection and attention of "
                          "the Llama-shaped layer from 4k to 128k tokens over a gamma sweep "
@@ -89,7 +91,8 @@ def time_loop(fn, steps, stream):
     return ev[0].elapsed_time(ev[1]) / steps
 
 
-def cpu_baseline(layer, spec, gamma, n_heads, n_rows, max_budget=0, qa_mode=0):
+def cpu_baseline(layer, spec, gamma, n_heads, n_rows, max_budget=0, qa_mode=0,
+                 vs_granularity=0):
     """Oracle on host cores over a bounded sample of the same layer, scaled to ms/layer:
     selection of `n_heads` whole heads, attention on `n_rows` random query-block rows of
     each of them; per-head and per-row means are scaled to all heads and rows."""
@@ -115,7 +118,8 @@ def cpu_baseline(layer, spec, gamma, n_heads, n_rows, max_budget=0, qa_mode=0):
         qs, ks, vs = layer.q[t0:t1, h], layer.k[t0:t1, h // G], layer.v[t0:t1, h // G]
         t = time.perf_counter()
         r = oracle.select_head(qs, ks, b, gamma, spec.tau, spec.min_budget, scale,
-                               max_budget=max_budget, qa_mode=qa_mode)
+                               max_budget=max_budget, qa_mode=qa_mode,
+                               vs_granularity=vs_granularity)
         t_sel += time.perf_counter() - t
         nb = r["mask"].shape[0]
         rows = rng.choice(nb, size=min(n_rows, nb), replace=False)
@@ -171,14 +175,15 @@ def sweep(args):
         del idx_d
         for gamma in SWEEP_GAMMAS:
             p = fpx.params(gamma, spec.tau, spec.min_budget, qa_mode=args.qa_mode,
-                           max_budget=args.max_budget)
+                           max_budget=args.max_budget, vs_granularity=args.vs_granularity)
             ws_sel = torch.empty(max(fpx.select_workspace_size(shape, p), 1), dtype=torch.uint8,
                                  device=dev)
             idx = fpx.empty_indices(shape, dev)
 
             def sel():
                 fpx.select(q, k, cu, gamma, spec.tau, spec.min_budget, out=idx, workspace=ws_sel,
-                           qa_mode=args.qa_mode, max_budget=args.max_budget)
+                           qa_mode=args.qa_mode, max_budget=args.max_budget,
+                           vs_granularity=args.vs_granularity)
 
             def att():
                 fpx.sparse_attn(q, k, v, idx, out=o, workspace=ws_att)
@@ -204,6 +209,7 @@ def sweep(args):
         torch.cuda.empty_cache()
     table = {"workload": "llama3-8b-layer, 32/8 heads, d 128, tau 0.1, min budget 8 blocks",
              "qa_mode": args.qa_mode, "max_budget_blocks": args.max_budget,
+             "vs_granularity": args.vs_granularity,
              "data": "synthetic (seeded vertical-slash / clustered heads, bf16)", "rows": rows}
     with open(args.sweep, "w") as f:
         json.dump(table, f, indent=1)
@@ -248,7 +254,8 @@ def main():
     cu = layer.cu_seqlens
     stream = torch.cuda.current_stream()
     shape = fpx.Shape(cu, spec.hq, spec.hkv, spec.d, spec.block)
-    sel_kw = dict(max_budget=args.max_budget, qa_mode=args.qa_mode)
+    sel_kw = dict(max_budget=args.max_budget, qa_mode=args.qa_mode,
+                  vs_granularity=args.vs_granularity)
     p = fpx.params(gamma, spec.tau, spec.min_budget, **sel_kw)
     ws_sel = torch.empty(max(fpx.select_workspace_size(shape, p), 1), dtype=torch.uint8,
                          device=dev)
@@ -334,7 +341,8 @@ def main():
         "config": {"workload": spec.name, "seqlens": list(map(int, seqlens)), "q_heads": spec.hq,
                    "kv_heads": spec.hkv, "head_dim": spec.d, "block": spec.block,
                    "gamma": gamma, "tau": spec.tau, "min_budget_blocks": spec.min_budget,
-                   "max_budget_blocks": args.max_budget, "qa_mode": args.qa_mode},
+                   "max_budget_blocks": args.max_budget, "qa_mode": args.qa_mode,
+                   "vs_granularity": args.vs_granularity},
         "select_ms": round(ms_select, 4),
         "attn_ms": round(ms_attn, 4),
         "effective_tflops": round(f_dense / (ms_step * 1e-3) / 1e12, 2),

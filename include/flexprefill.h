@@ -78,7 +78,8 @@ typedef struct fp_params {
                               /* map (Algorithm 4); 1 per query block, each row of    */
                               /* the map reaching gamma (appendix "flatten ablation") */
   int32_t vs_granularity;     /* vertical-slash lines: 0 token lines (Algorithm 3);   */
-                              /* 1 block-pooled lines (reserved: FP_ERR_UNSUPPORTED)  */
+                              /* 1 block-pooled: key blocks and offset blocks of      */
+                              /* lines are the selection units                        */
 } fp_params;
 
 /* Outputs of fp_select (caller-allocated device buffers; sizes from fp_indices_size).
@@ -93,7 +94,8 @@ typedef struct fp_params {
  *   js     : float [batch * Hq], D_JS per (s, h) (negative when not computed).
  *   units  : int32 [batch * Hq * 2], per (s, h): {K, 0} for query-aware heads (units
  *            selected by Algorithm 4; with qa_mode 1 the sum over query blocks of
- *            their K), {K_v, K_s} for vertical-slash heads, {all, 0} when dense.
+ *            their K), {K_v, K_s} for vertical-slash heads (lines, or blocks of lines
+ *            with vs_granularity 1), {all, 0} when dense.
  *            Diagnostics only. */
 typedef struct fp_indices {
   int32_t *kb_idx;

@@ -84,7 +84,6 @@ fp_status check_params(const fp_shape *sh, const fp_params *p) {
     return FP_ERR_INVALID_ARG;
   if (p->qa_mode < 0 || p->qa_mode > 1) return FP_ERR_INVALID_ARG;
   if (p->vs_granularity < 0 || p->vs_granularity > 1) return FP_ERR_INVALID_ARG;
-  if (p->vs_granularity == 1) return FP_ERR_UNSUPPORTED;
   (void)sh;
   return FP_OK;
 }
@@ -105,6 +104,8 @@ size_t select_layout(const fp_shape *sh, const Dims &dm, char *base, fp::SelectA
   char *qbar = take(sizeof(float) * dm.nb_total * hq * d);
   char *a_v = take(sizeof(float) * hq * dm.total_tokens);
   char *a_s = take(sizeof(float) * hq * dm.total_tokens);
+  char *av_blk = take(sizeof(float) * hq * dm.nb_total);
+  char *as_blk = take(sizeof(float) * hq * dm.nb_total);
   char *flat = take(sizeof(float) * hq * dm.tri_total);
   char *sel = take(sizeof(fp::SelState) * problems);
   char *hist_cnt = take(sizeof(uint32_t) * problems * fp::kHistBuckets);
@@ -116,6 +117,8 @@ size_t select_layout(const fp_shape *sh, const Dims &dm, char *base, fp::SelectA
     a->qbar = (float *)qbar;
     a->a_v = (float *)a_v;
     a->a_s = (float *)a_s;
+    a->av_blk = (float *)av_blk;
+    a->as_blk = (float *)as_blk;
     a->flat = (float *)flat;
     a->sel = (fp::SelState *)sel;
     a->hist_cnt = (uint32_t *)hist_cnt;
@@ -211,6 +214,7 @@ fp_status fp_select(const fp_shape *shape, const void *q, const void *k, const f
   a.force_pattern = params->force_pattern;
   a.max_budget = params->max_budget_blocks;
   a.qa_mode = params->qa_mode;
+  a.vs_granularity = params->vs_granularity;
   a.kb_idx = out->kb_idx;
   a.kb_cnt = out->kb_cnt;
   a.pattern = out->pattern;

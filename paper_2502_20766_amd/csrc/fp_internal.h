@@ -38,6 +38,7 @@ struct SelectArgs {
   int32_t force_pattern;
   int32_t max_budget;      // 0 = no cap
   int32_t qa_mode;         // 0 flattened map (Algorithm 4), 1 per query block
+  int32_t vs_granularity;  // 0 token lines (Algorithm 3), 1 block-pooled lines
   // workspace
   float2 *chunk_stats;     // [ch_total][Hq][block] (max, sum) in log2 units
   float2 *row_stats;       // [n_seq][Hq][block]
@@ -45,6 +46,8 @@ struct SelectArgs {
   float *qbar;             // [NB][Hq][d]
   float *a_v;              // [Hq][T]
   float *a_s;              // [Hq][T]
+  float *av_blk;           // [Hq][NB] a_v summed per key block (block-pooled lines)
+  float *as_blk;           // [Hq][NB] a_s summed per offset block
   float *flat;             // [Hq][TRI]
   struct SelState *sel;    // [n_seq][Hq][2]
   uint32_t *hist_cnt;      // [n_seq][Hq][2][kHistBuckets]

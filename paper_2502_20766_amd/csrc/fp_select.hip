@@ -22,7 +22,9 @@
 // maximum budget M, rows above M blocks keep 0, I and their other blocks in that same
 // order (appendix "maximum budget limit").  Query-aware heads may instead select per query
 // block (appendix "flatten ablation"); those rows, and capped query-aware rows, are
-// finished by qa_rows.
+// finished by qa_rows.  With block-pooled lines the vertical-slash units are key blocks
+// and offset blocks of lines (pool_lines), and a selected unit marks the tiles of all its
+// lines.
 #include "fp_internal.h"
 
 namespace fp {
@@ -56,7 +58,11 @@ __device__ __forceinline__ Problem problem_of(const SelectArgs &a, int p) {
   const int tok0 = a.st.cu[s];
   const int n = a.st.cu[s + 1] - tok0;
   Problem pr{nullptr, 0, false};
-  if (pat == FP_PATTERN_VERTICAL_SLASH) {
+  if (pat == FP_PATTERN_VERTICAL_SLASH && a.vs_granularity == 1) {
+    pr.scores = (kind == 0 ? a.av_blk : a.as_blk) + (int64_t)h * a.nb_total + a.st.nb_off[s];
+    pr.n = a.st.nb_off[s + 1] - a.st.nb_off[s];
+    pr.active = true;
+  } else if (pat == FP_PATTERN_VERTICAL_SLASH) {
     pr.scores = (kind == 0 ? a.a_v : a.a_s) + (int64_t)h * a.total_tokens + tok0;
     pr.n = n;
     pr.active = true;
@@ -288,15 +294,31 @@ __global__ __launch_bounds__(1024) void convert_tiles(SelectArgs a) {
       d1[i] = 0;
     }
     __syncthreads();
-    const float *av = a.a_v + (int64_t)h * a.total_tokens + tok0;
-    const float *as = a.a_s + (int64_t)h * a.total_tokens + tok0;
-    for (int j = tid; j < n; j += blockDim.x) {
-      if (is_selected(S0, av[j], j)) colsel[j / b] = 1;
-      if (is_selected(S1, as[j], j)) {
-        const int dl = j / b, t = j % b;
-        d0[dl] = 1;
-        if (t < last_rows) d0p[dl] = 1;
-        if (t > 0) d1[dl + 1] = 1;
+    if (a.vs_granularity == 1) {
+      // a selected unit selects all its lines: key block J is a column; offset block D
+      // holds o = D*b (t = 0: diagonal D in every row) and, when it has more than one
+      // offset, o = D*b + t with t > 0 (diagonal D + 1)
+      const float *avb = a.av_blk + (int64_t)h * a.nb_total + a.st.nb_off[s];
+      const float *asb = a.as_blk + (int64_t)h * a.nb_total + a.st.nb_off[s];
+      for (int u = tid; u < nb; u += blockDim.x) {
+        if (is_selected(S0, avb[u], u)) colsel[u] = 1;
+        if (is_selected(S1, asb[u], u)) {
+          d0[u] = 1;
+          d0p[u] = 1;
+          if (n - u * b > 1) d1[u + 1] = 1;
+        }
+      }
+    } else {
+      const float *av = a.a_v + (int64_t)h * a.total_tokens + tok0;
+      const float *as = a.a_s + (int64_t)h * a.total_tokens + tok0;
+      for (int j = tid; j < n; j += blockDim.x) {
+        if (is_selected(S0, av[j], j)) colsel[j / b] = 1;
+        if (is_selected(S1, as[j], j)) {
+          const int dl = j / b, t = j % b;
+          d0[dl] = 1;
+          if (t < last_rows) d0p[dl] = 1;
+          if (t > 0) d1[dl + 1] = 1;
+        }
       }
     }
     __syncthreads();
@@ -413,6 +435,37 @@ __global__ __launch_bounds__(1024) void convert_tiles(SelectArgs a) {
       running += __popcll(bal);
     }
     if (lane == 0) a.kb_cnt[(int64_t)h * a.nb_total + a.st.nb_off[s] + I] = running;
+  }
+}
+
+// Block-pooled lines: a_v summed over each key block and a_s over each offset block, one
+// wave per (query head, block); vertical-slash heads only.
+__global__ __launch_bounds__(256) void pool_lines(SelectArgs a) {
+  const int h = blockIdx.y;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= a.nb_total) return;
+  int s = 0;
+  while (s + 1 < a.st.n_seq && a.st.nb_off[s + 1] <= row) ++s;
+  if (a.pattern[s * a.hq + h] != FP_PATTERN_VERTICAL_SLASH) return;
+  const int u = row - a.st.nb_off[s];
+  const int tok0 = a.st.cu[s];
+  const int n = a.st.cu[s + 1] - tok0;
+  const int lo = u * a.block, hi = min(lo + a.block, n);
+  const float *av = a.a_v + (int64_t)h * a.total_tokens + tok0;
+  const float *as = a.a_s + (int64_t)h * a.total_tokens + tok0;
+  float sv = 0.f, ss = 0.f;
+  for (int j = lo + lane; j < hi; j += 64) {
+    sv += av[j];
+    ss += as[j];
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    sv += __shfl_xor(sv, off);
+    ss += __shfl_xor(ss, off);
+  }
+  if (lane == 0) {
+    a.av_blk[(int64_t)h * a.nb_total + row] = sv;
+    a.as_blk[(int64_t)h * a.nb_total + row] = ss;
   }
 }
 
@@ -607,6 +660,8 @@ hipError_t launch_select_pipeline(const SelectArgs &a, hipStream_t stream) {
     max_units = max(max_units, max(n, nb * (nb + 1) / 2));
   }
   const int slices = (max_units + kSlice - 1) / kSlice;
+  if (a.vs_granularity == 1)
+    hipLaunchKernelGGL(pool_lines, dim3((a.nb_total + 3) / 4, a.hq), dim3(256), 0, stream, a);
   hipLaunchKernelGGL(sel_init, dim3(problems), dim3(256), 0, stream, a);
   hipLaunchKernelGGL(sel_hist<0>, dim3(slices, problems), dim3(256), 0, stream, a);
   hipLaunchKernelGGL(sel_scan<0>, dim3(problems), dim3(256), 0, stream, a);

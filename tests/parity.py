@@ -54,7 +54,7 @@ def allowed_cuts(sel: ofp.Selection, gamma: float, band: float = BAND):
 
 
 def expected_mask_for_cuts(q_seq, k_seq, block, gamma, min_budget, scale, pattern, detail, cuts,
-                           n, max_budget=0):
+                           n, max_budget=0, vs_granularity=0):
     """Rebuild the oracle's block mask for the given cut points (oracle functions only)."""
     nb = -(-n // block)
     if pattern == oracle.PATTERN_QA:
@@ -65,7 +65,10 @@ def expected_mask_for_cuts(q_seq, k_seq, block, gamma, min_budget, scale, patter
                                                 detail["a_map"])
         return oracle.apply_max_budget(mask, oracle.PATTERN_QA, max_budget, detail["a_map"])
     sv, ss = detail["v"], detail["s"]
-    mask = oracle.tiles_from_vertical_slash(sv.order[:cuts[0]], ss.order[:cuts[1]], n, block)
+    vl, sl = sv.order[:cuts[0]], ss.order[:cuts[1]]
+    if vs_granularity == 1:
+        vl, sl = oracle.lines_of_blocks(vl, n, block), oracle.lines_of_blocks(sl, n, block)
+    mask = oracle.tiles_from_vertical_slash(vl, sl, n, block)
     mask = oracle.add_forced_and_min_budget(mask, oracle.PATTERN_VS, min_budget)
     return oracle.apply_max_budget(mask, oracle.PATTERN_VS, max_budget)
 
@@ -95,7 +98,7 @@ def order_tie_ok(dev_row, exp_row, a_map, I, rel=1e-5):
 
 
 def compare_selection(layer, gpu, gamma, tau, min_budget, heads=None, scale=None,
-                      max_budget=0, qa_mode=0):
+                      max_budget=0, qa_mode=0, vs_granularity=0):
     """gpu: dict with 'masks' {(s,h): bool[nb,nb]}, 'pattern' [B*Hq], 'js' [B*Hq],
     'units' [B*Hq*2] (host arrays).  Returns statistics; raises AssertionError on a
     mismatch that the bands do not explain.  With qa_mode 1 every query-aware row is its
@@ -117,7 +120,7 @@ def compare_selection(layer, gpu, gamma, tau, min_budget, heads=None, scale=None
                 continue
             qs, ks = layer.q[t0:t1, h], layer.k[t0:t1, h // G]
             o = oracle.select_head(qs, ks, spec.block, gamma, tau, min_budget, scale, -1, True,
-                                   max_budget, qa_mode)
+                                   max_budget, qa_mode, vs_granularity)
             gp = int(gpu["pattern"][s * hq + h])
             gm = gpu["masks"][(s, h)]
             stats["heads"] += 1
@@ -132,7 +135,7 @@ def compare_selection(layer, gpu, gamma, tau, min_budget, heads=None, scale=None
                 stats["pattern_boundary"] += 1
                 if gp != o["pattern"]:
                     o = oracle.select_head(qs, ks, spec.block, gamma, tau, min_budget, scale, gp,
-                                           True, max_budget, qa_mode)
+                                           True, max_budget, qa_mode, vs_granularity)
             assert gp == o["pattern"], f"pattern s={s} h={h}: gpu {gp} oracle {o['pattern']} " \
                                        f"js {o['js']:.6f} tau {tau}"
             det = o["detail"]
@@ -175,7 +178,7 @@ def compare_selection(layer, gpu, gamma, tau, min_budget, heads=None, scale=None
             if cuts != oracle_cuts:
                 stats["boundary_problems"] += sum(int(a != b) for a, b in zip(cuts, oracle_cuts))
                 exp = expected_mask_for_cuts(qs, ks, spec.block, gamma, min_budget, scale, gp, det,
-                                             cuts, n, max_budget)
+                                             cuts, n, max_budget, vs_granularity)
             else:
                 exp = o["mask"]
                 stats["exact_heads"] += 1

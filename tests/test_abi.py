@@ -99,7 +99,8 @@ def test_validate_shape_errors(lib, kw, status):
     (dict(gamma=0.9, tau=0.1, qa_mode=2), fpx.FP_ERR_INVALID_ARG),
     (dict(gamma=0.9, tau=0.1, qa_mode=1), fpx.FP_OK),
     (dict(gamma=0.9, tau=0.1, vs_granularity=-1), fpx.FP_ERR_INVALID_ARG),
-    (dict(gamma=0.9, tau=0.1, vs_granularity=1), fpx.FP_ERR_UNSUPPORTED),
+    (dict(gamma=0.9, tau=0.1, vs_granularity=2), fpx.FP_ERR_INVALID_ARG),
+    (dict(gamma=0.9, tau=0.1, vs_granularity=1), fpx.FP_OK),
     (dict(gamma=0.9, tau=0.1), fpx.FP_OK),
     (dict(gamma=1.0, tau=0.0, min_budget=64, force_pattern=1), fpx.FP_OK),
 ])

@@ -30,11 +30,12 @@ def _fpx():
     return fpx
 
 
-def run_gpu(layer, gamma, tau, min_budget, force_pattern=-1, max_budget=0, qa_mode=0):
+def run_gpu(layer, gamma, tau, min_budget, force_pattern=-1, max_budget=0, qa_mode=0,
+            vs_granularity=0):
     fpx = _fpx()
     q, k, v = to_device(layer)
     idx = fpx.select(q, k, layer.cu_seqlens, gamma, tau, min_budget, force_pattern=force_pattern,
-                     max_budget=max_budget, qa_mode=qa_mode)
+                     max_budget=max_budget, qa_mode=qa_mode, vs_granularity=vs_granularity)
     o = fpx.sparse_attn(q, k, v, idx)
     torch.cuda.synchronize()
     return dict(masks=fpx.masks_from_indices(idx), pattern=idx.pattern.cpu().numpy(),
@@ -219,31 +220,37 @@ RAGGED = synth.SPECS["qwen_varlen"].with_seqlens((300, 129, 1, 2000, 4096), "rag
 GLM = synth.SPECS["glm64k"].with_seqlens((8192,), "glm-gqa16-n8192")
 
 VARIANT_CASES = [
-    # (name, spec, qa_mode, max_budget, min_budget or None = the spec's)
-    ("rows-mixed-8h-n8192", MIXED, 1, 0, None),
-    ("rows-ragged-varlen", RAGGED, 1, 0, None),
-    ("rows-glm-gqa16-n8192", GLM, 1, 0, None),
-    ("cap16-mixed-8h-n8192", MIXED, 0, 16, None),
-    ("rows-cap12-mixed-8h-n8192", MIXED, 1, 12, None),
-    ("cap2-ragged-varlen", RAGGED, 0, 2, 1),
-    ("rows-cap9-glm-gqa16-n8192", GLM, 1, 9, None),
+    # (name, spec, qa_mode, max_budget, min_budget or None = the spec's, vs_granularity)
+    ("rows-mixed-8h-n8192", MIXED, 1, 0, None, 0),
+    ("rows-ragged-varlen", RAGGED, 1, 0, None, 0),
+    ("rows-glm-gqa16-n8192", GLM, 1, 0, None, 0),
+    ("cap16-mixed-8h-n8192", MIXED, 0, 16, None, 0),
+    ("rows-cap12-mixed-8h-n8192", MIXED, 1, 12, None, 0),
+    ("cap2-ragged-varlen", RAGGED, 0, 2, 1, 0),
+    ("rows-cap9-glm-gqa16-n8192", GLM, 1, 9, None, 0),
+    ("pooled-mixed-8h-n8192", MIXED, 0, 0, None, 1),
+    ("pooled-ragged-varlen", RAGGED, 0, 0, None, 1),
+    ("pooled-rows-cap10-mixed-8h-n8192", MIXED, 1, 10, None, 1),
 ]
 
 
 @pytest.mark.parametrize("case", VARIANT_CASES, ids=[c[0] for c in VARIANT_CASES])
 def test_query_wise_selection_and_max_budget_vs_oracle(case):
-    """Per-query-block query-aware selection and the per-row cap, against the oracle."""
-    name, spec, qa_mode, max_budget, mb = case
+    """Per-query-block query-aware selection, the per-row cap and block-pooled
+    vertical-slash lines, against the oracle."""
+    name, spec, qa_mode, max_budget, mb, vsg = case
     min_budget = spec.min_budget if mb is None else mb
-    log(f"[selection variant] {name} qa_mode={qa_mode} max_budget={max_budget} m={min_budget}")
+    log(f"[selection variant] {name} qa_mode={qa_mode} max_budget={max_budget} m={min_budget} "
+        f"vs_granularity={vsg}")
     layer = synth.make_layer(spec)
-    g = run_gpu(layer, spec.gamma, spec.tau, min_budget, max_budget=max_budget, qa_mode=qa_mode)
+    g = run_gpu(layer, spec.gamma, spec.tau, min_budget, max_budget=max_budget, qa_mode=qa_mode,
+                vs_granularity=vsg)
     check_lists_structure(g["idx"], layer, min_budget)
     if max_budget:
         assert int(g["idx"].kb_cnt.max()) <= max_budget
     with Timer("oracle selection"):
         st = compare_selection(layer, g, spec.gamma, spec.tau, min_budget,
-                               max_budget=max_budget, qa_mode=qa_mode)
+                               max_budget=max_budget, qa_mode=qa_mode, vs_granularity=vsg)
     log(f"  {st}")
     assert st["order_ties"] <= max(2, st["heads"])        # rare: float32 vs float64 ranks
     mx, mean = compare_outputs(layer, g["o"], g["masks"], rows_per_head=4)
