@@ -62,6 +62,8 @@ def parse():
                     help="query-aware selection: 0 flattened map (Algorithm 4), 1 per query block")
     ap.add_argument("--max-budget", type=int, default=0,
                     help="per-row cap in key blocks (0 = none)")
+    ap.add_argument("--block", type=int, default=None,
+                    help="block size (128 or 64); default: the workload's (128)")
     ap.add_argument("--vs-granularity", type=int, default=0,
                     help="vertical-slash lines: 0 token lines (Algorithm 3), 1 block-pooled")
     ap.add_argument("--sweep", default=None, metavar="OUT.json",
@@ -168,7 +170,7 @@ def sweep(args):
         nb = -(-n // spec.block)
         causal_tiles = spec.hq * nb * (nb + 1) // 2
         reps = max(3, min(20, int(2e5 // n)))
-        idx_d = fpx.select(q, k, cu, 1.0, spec.tau, spec.min_budget)
+        idx_d = fpx.select(q, k, cu, 1.0, spec.tau, spec.min_budget, block=spec.block)
         fpx.sparse_attn(q, k, v, idx_d, out=o, workspace=ws_att)
         ms_dense = time_loop(lambda: fpx.sparse_attn(q, k, v, idx_d, out=o, workspace=ws_att),
                              max(2, reps // 2), stream)
@@ -233,6 +235,8 @@ def main():
     import paper_2502_20766_amd as fpx
 
     spec = synth.SPECS[args.workload]
+    if args.block is not None and args.block != spec.block:
+        spec = spec.with_params(block=args.block)
     gamma = spec.gamma if args.gamma is None else args.gamma
     log(f"[bench] generating {spec.name} (seqlens {spec.seqlens}, {spec.hq}/{spec.hkv} heads, "
         f"d {spec.d})")
@@ -264,8 +268,8 @@ def main():
     o = torch.empty_like(q)
 
     def do_select():
-        fpx.select(q, k, cu, gamma, spec.tau, spec.min_budget, out=idx, workspace=ws_sel,
-                   **sel_kw)
+        fpx.select(q, k, cu, gamma, spec.tau, spec.min_budget, block=spec.block, out=idx,
+                   workspace=ws_sel, **sel_kw)
 
     def do_attn():
         fpx.sparse_attn(q, k, v, idx, out=o, workspace=ws_att)
@@ -295,7 +299,7 @@ def main():
 
     dense = {}
     if not args.no_dense:
-        idx_d = fpx.select(q, k, cu, 1.0, spec.tau, spec.min_budget)
+        idx_d = fpx.select(q, k, cu, 1.0, spec.tau, spec.min_budget, block=spec.block)
         fpx.sparse_attn(q, k, v, idx_d, out=o, workspace=ws_att)
         ms_dense_lib = time_loop(lambda: fpx.sparse_attn(q, k, v, idx_d, out=o,
                                                          workspace=ws_att), max(2, args.steps // 3),
@@ -357,7 +361,7 @@ def main():
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": attn_traffic_bytes(spec.name),
-                     "kernel": "sparse_fa_fwd<128>",
+                     "kernel": f"sparse_fa_fwd<{spec.d}, {spec.block}>",
                      "per_launch_flop": f_comp},
     }
     if not args.no_cpu_baseline:

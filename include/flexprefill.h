@@ -58,7 +58,8 @@ typedef struct fp_shape {
   int32_t num_q_heads;        /* Hq >= 1                                              */
   int32_t num_kv_heads;       /* Hkv >= 1, Hq % Hkv == 0                              */
   int32_t head_dim;           /* d in {64, 128}                                       */
-  int32_t block;              /* block_size; 128 (the paper's setting, Section 4.1)  */
+  int32_t block;              /* block_size: 128 (the paper's setting, Section 4.1)  */
+                              /* or 64; at most 8192 blocks per sequence             */
 } fp_shape;
 
 /* Method parameters (Algorithm 1 inputs tau, gamma; Section 4.1 guards). */

@@ -32,7 +32,7 @@ fp_status check_shape(const fp_shape *sh, Dims *dm) {
   if (sh->num_q_heads % sh->num_kv_heads != 0) return FP_ERR_INVALID_ARG;
   if (sh->batch > FP_MAX_BATCH) return FP_ERR_UNSUPPORTED;
   if (sh->head_dim != 64 && sh->head_dim != 128) return FP_ERR_UNSUPPORTED;
-  if (sh->block != 128) return FP_ERR_UNSUPPORTED;
+  if (sh->block != 128 && sh->block != 64) return FP_ERR_UNSUPPORTED;
   if (sh->num_kv_heads > 1024 || sh->num_q_heads > 8192) return FP_ERR_UNSUPPORTED;
   if (sh->cu_seqlens[0] != 0) return FP_ERR_INVALID_ARG;
   memset(dm, 0, sizeof(*dm));
@@ -44,7 +44,7 @@ fp_status check_shape(const fp_shape *sh, Dims *dm) {
     const int64_t n = (int64_t)sh->cu_seqlens[s + 1] - sh->cu_seqlens[s];
     if (n < 1) return FP_ERR_INVALID_ARG;
     const int64_t nb = (n + sh->block - 1) / sh->block;
-    if (nb > 8192) return FP_ERR_UNSUPPORTED;        // sequences up to 1M tokens
+    if (nb > 8192) return FP_ERR_UNSUPPORTED;   // up to 1M tokens (512k at block 64)
     st.cu[s] = sh->cu_seqlens[s];
     st.nb_off[s] = (int32_t)nb_acc;
     st.tri_off[s] = tri_acc;

@@ -35,9 +35,17 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int BM = 128;  // queries per workgroup (one query block)
-constexpr int BN = 128;  // keys per tile (one key block)
-constexpr int kThreads = 256;
+// Block size B (queries per query block = keys per key block) is 128 or 64.  A workgroup
+// is one query block: B/32 waves of 32 query rows.  Keys go through LDS in stages of B/2
+// keys (two stages per key block), each stage made of 32-key MFMA sub-blocks.
+template <int B>
+struct Geo {
+  static constexpr int WAVES = B / 32;
+  static constexpr int THREADS = 64 * WAVES;
+  static constexpr int KEYS = B / 2;            // keys per stage
+  static constexpr int SUB = KEYS / 32;         // 32-key sub-blocks per stage
+  static constexpr int WG_PER_CU = 512 / THREADS;  // two waves per SIMD
+};
 
 __device__ __forceinline__ float wave_pair_max(float x) {
   // lanes l and l^32 exchange values; max of both halves of the swap is symmetric
@@ -50,15 +58,15 @@ __device__ __forceinline__ float wave_pair_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Geometry of one 64-key stage in LDS (K and V both row-major [key][d], bf16).
-template <int D>
+// Geometry of one stage in LDS (K and V both row-major [key][d], bf16).
+template <int D, int B>
 struct Stage {
   static constexpr int RB = 2 * D;                 // bytes per key row
   static constexpr int CPR = RB / 16;              // 16-byte chunks per row
-  static constexpr int KEYS = 64;
+  static constexpr int KEYS = Geo<B>::KEYS;
   static constexpr int BYTES = KEYS * RB;          // one tile (K or V)
   static constexpr int RPI = 1024 / RB;            // rows written by one wave-wide DMA
-  static constexpr int DMA_PER_WAVE = BYTES / 1024 / 4;
+  static constexpr int DMA_PER_WAVE = BYTES / 1024 / Geo<B>::WAVES;
 };
 
 // 16-byte chunk swizzles (XOR, so the same function maps logical <-> physical).
@@ -76,21 +84,21 @@ __device__ __forceinline__ int swz_v(int y, int r) {
 }
 
 // Per-lane byte offsets of the DMA slots of one stage, relative to the stage's first key
-// row: slot i of wave w covers LDS bytes [(4i + w) * 1024, +1024), lane l fills 16 bytes
-// of tile row r with the logical chunk whose swizzled position is the lane's slot.
-template <int D>
+// row: slot i of wave w covers LDS bytes [(WAVES i + w) * 1024, +1024), lane l fills 16
+// bytes of tile row r with the logical chunk whose swizzled position is the lane's slot.
+template <int D, int B>
 struct DmaOffsets {
-  uint32_t k[Stage<D>::DMA_PER_WAVE];
-  uint32_t v[Stage<D>::DMA_PER_WAVE];
+  uint32_t k[Stage<D, B>::DMA_PER_WAVE];
+  uint32_t v[Stage<D, B>::DMA_PER_WAVE];
 };
 
-template <int D>
-__device__ __forceinline__ DmaOffsets<D> dma_offsets(uint32_t row_bytes, int w, int lane) {
-  using S = Stage<D>;
-  DmaOffsets<D> o;
+template <int D, int B>
+__device__ __forceinline__ DmaOffsets<D, B> dma_offsets(uint32_t row_bytes, int w, int lane) {
+  using S = Stage<D, B>;
+  DmaOffsets<D, B> o;
 #pragma unroll
   for (int i = 0; i < S::DMA_PER_WAVE; ++i) {
-    const int r = (i * 4 + w) * S::RPI + lane / S::CPR;
+    const int r = (i * Geo<B>::WAVES + w) * S::RPI + lane / S::CPR;
     const int phys = lane % S::CPR;
     o.k[i] = r * row_bytes + swz_k<D>(phys, r) * 16;
     o.v[i] = r * row_bytes + swz_v<D>(phys, r) * 16;
@@ -111,21 +119,21 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void *base,
                                            0x00020000);
 }
 
-// Issue the DMA of one 64-key stage: keys k0 .. k0+63 of the sequence through buffer
+// Issue the DMA of one stage: keys k0 .. k0+KEYS-1 of the sequence through buffer
 // descriptors whose range ends at the last valid key row, so rows past the sequence end
 // read as zeros (and are masked by the caller).
-template <int D>
+template <int D, int B>
 __device__ __forceinline__ void stage_dma(uint8_t *ks, uint8_t *vs, const uint16_t *kbase,
                                           const uint16_t *vbase, int64_t kv_row, int k0,
-                                          int kvalid, const DmaOffsets<D> &off) {
-  using S = Stage<D>;
+                                          int kvalid, const DmaOffsets<D, B> &off) {
+  using S = Stage<D, B>;
   const int nrec = (kvalid - 1) * (int)kv_row * 2 + 2 * D;
   const __amdgpu_buffer_rsrc_t rk = uniform_rsrc(kbase + (int64_t)k0 * kv_row, nrec);
   const __amdgpu_buffer_rsrc_t rv = uniform_rsrc(vbase + (int64_t)k0 * kv_row, nrec);
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
   for (int i = 0; i < S::DMA_PER_WAVE; ++i) {
-    const int q = i * 4 + w;
+    const int q = i * Geo<B>::WAVES + w;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
         rk, (__attribute__((address_space(3))) void *)(ks + q * 1024), 16, off.k[i], 0, 0, 0);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
@@ -256,9 +264,10 @@ __device__ __forceinline__ Row uniform_row(const Row &r) {
 }
 
 // First key of stage `half` of key block J in row r, or -1 when the stage has no keys.
+template <int B>
 __device__ __forceinline__ int stage_first_key(const Row &r, int J, int half) {
   if (J < 0 || J > r.I) return -1;
-  const int k0 = J * BN + 64 * half;
+  const int k0 = J * B + Geo<B>::KEYS * half;
   return k0 < r.n ? k0 : -1;
 }
 
@@ -270,10 +279,11 @@ __device__ __forceinline__ int stage_first_key(const Row &r, int J, int half) {
 // stages (one dependent step per stage, each step's loads covered by the wait for the
 // stage's K/V copy) and its first K/V copy is issued at the top of the current row's last
 // stage.
-template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+template <int D, int B>
+__global__ __launch_bounds__(Geo<B>::THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void sparse_fa_fwd(AttnArgs a) {
-  using S = Stage<D>;
+  using S = Stage<D, B>;
+  constexpr int BM = B;                   // queries per workgroup (one query block)
   constexpr int KS = D / 16;
   constexpr int DB = D / 32;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[4 * S::BYTES];  // [2 stages][K, V]
@@ -415,7 +425,7 @@ void sparse_fa_fwd(AttnArgs a) {
     for (int k = 0; k < KS; ++k) qf[k] = *reinterpret_cast<const bf16x8 *>(qp + 16 * k);
   };
 
-  const DmaOffsets<D> doff = dma_offsets<D>((uint32_t)(kv_row * 2), w, lane);
+  const DmaOffsets<D, B> doff = dma_offsets<D, B>((uint32_t)(kv_row * 2), w, lane);
   // per-lane V^T fragment addresses (relative to a V stage), one per d-block
   uint32_t vaddr_rel[DB];
   {
@@ -436,7 +446,7 @@ void sparse_fa_fwd(AttnArgs a) {
     const uint16_t *kb = a.k + (int64_t)r.tok0 * kv_row + (int64_t)r.g * D;
     const uint16_t *vbp = a.v + (int64_t)r.tok0 * kv_row + (int64_t)r.g * D;
     uint8_t *dst = lds + into * 2 * S::BYTES;
-    stage_dma<D>(dst, dst + S::BYTES, kb, vbp, kv_row, k0, min(64, r.n - k0), doff);
+    stage_dma<D, B>(dst, dst + S::BYTES, kb, vbp, kv_row, k0, min(S::KEYS, r.n - k0), doff);
   };
 
   if (!cur.valid) {                       // this XCD's queue had no first item: take one
@@ -449,7 +459,7 @@ void sparse_fa_fwd(AttnArgs a) {
     nxt.valid = 0;
   }
   int buf = 0;
-  int k0_next = stage_first_key(cur, cur.J0, 0);
+  int k0_next = stage_first_key<B>(cur, cur.J0, 0);
   if (k0_next >= 0) issue(cur, k0_next, buf);
   bf16x8 qf[KS];
   while (true) {
@@ -487,17 +497,17 @@ void sparse_fa_fwd(AttnArgs a) {
       k0_next = -1;
       if (t + 1 < 2 * cur.cnt) {
         if ((t & 1) == 0) {
-          k0_next = stage_first_key(cur, J_cur, 1);
+          k0_next = stage_first_key<B>(cur, J_cur, 1);
         } else {
           J_cur = J_pre;
           J_pre = ((t >> 1) + 2 < cur.cnt) ? cur.list[(t >> 1) + 2] : -1;
-          k0_next = stage_first_key(cur, J_cur, 0);
+          k0_next = stage_first_key<B>(cur, J_cur, 0);
         }
         if (k0_next >= 0) issue(cur, k0_next, buf ^ 1);
       } else {
         fetch_finish();
         if (nxt.valid) {
-          k0_next = stage_first_key(nxt, nxt.J0, 0);
+          k0_next = stage_first_key<B>(nxt, nxt.J0, 0);
           if (k0_next >= 0) issue(nxt, k0_next, buf ^ 1);
         }
       }
@@ -554,29 +564,6 @@ void sparse_fa_fwd(AttnArgs a) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) p0[v] = __builtin_amdgcn_exp2f(fmaf(sacc[0][v], c, -mc));
     };
-    // sub-block 0 scores and running max
-    qk_block(std::integral_constant<int, 0>{});
-    update_max(mask_max(0));
-    // sub-block 1 scores on MFMA while sub-block 0's weights are computed on VALU
-    qk_block(std::integral_constant<int, 1>{});
-    float p0[16];
-    weights0(p0);
-    // keep these exponentials here, beside sub-block 1's MFMAs (the compiler would
-    // otherwise sink them past the rescale branch below, next to their use)
-    asm volatile("" : "+v"(p0[0]), "+v"(p0[1]), "+v"(p0[2]), "+v"(p0[3]), "+v"(p0[4]),
-                 "+v"(p0[5]), "+v"(p0[6]), "+v"(p0[7]), "+v"(p0[8]), "+v"(p0[9]),
-                 "+v"(p0[10]), "+v"(p0[11]), "+v"(p0[12]), "+v"(p0[13]), "+v"(p0[14]),
-                 "+v"(p0[15]));
-    // sub-block 1 max; if the reference moved, sub-block 0's weights are recomputed
-    if (update_max(mask_max(1))) weights0(p0);
-    bf16x8 pf0[2];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      pf0[0][e] = (__bf16)p0[e];
-      pf0[1][e] = (__bf16)p0[8 + e];
-      l_run += p0[e] + p0[8 + e];
-    }
-
     // ---- O^T += V^T P^T, 16 keys per step; V^T fragments by transposing loads
     uint32_t va[DB];
 #pragma unroll
@@ -590,30 +577,73 @@ void sparse_fa_fwd(AttnArgs a) {
                                                            oacc[db], 0, 0, 0);
       }
     };
-    {
+    if constexpr (Geo<B>::SUB == 2) {
+      // sub-block 0 scores and running max
+      qk_block(std::integral_constant<int, 0>{});
+      update_max(mask_max(0));
+      // sub-block 1 scores on MFMA while sub-block 0's weights are computed on VALU
+      qk_block(std::integral_constant<int, 1>{});
+      float p0[16];
+      weights0(p0);
+      // keep these exponentials here, beside sub-block 1's MFMAs (the compiler would
+      // otherwise sink them past the rescale branch below, next to their use)
+      asm volatile("" : "+v"(p0[0]), "+v"(p0[1]), "+v"(p0[2]), "+v"(p0[3]), "+v"(p0[4]),
+                   "+v"(p0[5]), "+v"(p0[6]), "+v"(p0[7]), "+v"(p0[8]), "+v"(p0[9]),
+                   "+v"(p0[10]), "+v"(p0[11]), "+v"(p0[12]), "+v"(p0[13]), "+v"(p0[14]),
+                   "+v"(p0[15]));
+      // sub-block 1 max; if the reference moved, sub-block 0's weights are recomputed
+      if (update_max(mask_max(1))) weights0(p0);
+      bf16x8 pf0[2];
+  #pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        pf0[0][e] = (__bf16)p0[e];
+        pf0[1][e] = (__bf16)p0[8 + e];
+        l_run += p0[e] + p0[8 + e];
+      }
+
+      {
+        s16x4 vlo[DB], vhi[DB];
+        v_frags<DB, 0 * 16 * S::RB, 0 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
+        pv_step(pf0[0], vlo, vhi);
+        v_frags<DB, 1 * 16 * S::RB, 1 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
+        pv_step(pf0[1], vlo, vhi);
+      }
+      // sub-block 1 weights (VALU) overlap the PV MFMAs of sub-block 0
+      bf16x8 pf1[2];
+      {
+        const float mc = (m_ref == -INFINITY) ? 0.f : m_ref * c;
+  #pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(sacc[1][v], c, -mc));
+          pf1[v >> 3][v & 7] = (__bf16)p;
+          l_run += p;
+        }
+      }
+      {
+        s16x4 vlo[DB], vhi[DB];
+        v_frags<DB, 2 * 16 * S::RB, 2 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
+        pv_step(pf1[0], vlo, vhi);
+        v_frags<DB, 3 * 16 * S::RB, 3 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
+        pv_step(pf1[1], vlo, vhi);
+      }
+    } else {
+      // one 32-key sub-block per stage (block 64)
+      qk_block(std::integral_constant<int, 0>{});
+      update_max(mask_max(0));
+      float p0[16];
+      weights0(p0);
+      bf16x8 pf0[2];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        pf0[0][e] = (__bf16)p0[e];
+        pf0[1][e] = (__bf16)p0[8 + e];
+        l_run += p0[e] + p0[8 + e];
+      }
       s16x4 vlo[DB], vhi[DB];
       v_frags<DB, 0 * 16 * S::RB, 0 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
       pv_step(pf0[0], vlo, vhi);
       v_frags<DB, 1 * 16 * S::RB, 1 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
       pv_step(pf0[1], vlo, vhi);
-    }
-    // sub-block 1 weights (VALU) overlap the PV MFMAs of sub-block 0
-    bf16x8 pf1[2];
-    {
-      const float mc = (m_ref == -INFINITY) ? 0.f : m_ref * c;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[1][v], c, -mc));
-        pf1[v >> 3][v & 7] = (__bf16)p;
-        l_run += p;
-      }
-    }
-    {
-      s16x4 vlo[DB], vhi[DB];
-      v_frags<DB, 2 * 16 * S::RB, 2 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
-      pv_step(pf1[0], vlo, vhi);
-      v_frags<DB, 3 * 16 * S::RB, 3 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
-      pv_step(pf1[1], vlo, vhi);
     }
     }
 
@@ -770,8 +800,8 @@ hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t stream) {
     hipLaunchKernelGGL(build_item_order_plain, dim3((a.nb_total + 255) / 256), dim3(256), 0,
                        stream, a.st, a.kb_idx, a.kb_cnt, a.hq, a.hkv, a.tri_total, a.items,
                        a.queue);
-  // Persistent grid: two resident workgroups per CU (a multiple of 8, one share per XCD),
-  // no more than there are items.
+  // Persistent grid: resident workgroups for two waves per SIMD (a multiple of 8, one
+  // share per XCD), no more than there are items.
   static int cus = 0;
   if (cus == 0) {
     int dev = 0;
@@ -781,11 +811,24 @@ hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t stream) {
       cus = 256;
   }
   const int64_t total = n_g * a.hkv;
-  const int blocks = (int)std::min<int64_t>((2 * cus / 8) * 8, (total + 7) / 8 * 8);
-  if (a.d == 128)
-    hipLaunchKernelGGL(sparse_fa_fwd<128>, dim3(blocks), dim3(kThreads), 0, stream, a);
-  else
-    hipLaunchKernelGGL(sparse_fa_fwd<64>, dim3(blocks), dim3(kThreads), 0, stream, a);
+  auto grid = [&](int wg_per_cu) {
+    return (int)std::min<int64_t>((wg_per_cu * cus / 8) * 8, (total + 7) / 8 * 8);
+  };
+  if (a.block == 128) {
+    if (a.d == 128)
+      hipLaunchKernelGGL((sparse_fa_fwd<128, 128>), dim3(grid(Geo<128>::WG_PER_CU)),
+                         dim3(Geo<128>::THREADS), 0, stream, a);
+    else
+      hipLaunchKernelGGL((sparse_fa_fwd<64, 128>), dim3(grid(Geo<128>::WG_PER_CU)),
+                         dim3(Geo<128>::THREADS), 0, stream, a);
+  } else {
+    if (a.d == 128)
+      hipLaunchKernelGGL((sparse_fa_fwd<128, 64>), dim3(grid(Geo<64>::WG_PER_CU)),
+                         dim3(Geo<64>::THREADS), 0, stream, a);
+    else
+      hipLaunchKernelGGL((sparse_fa_fwd<64, 64>), dim3(grid(Geo<64>::WG_PER_CU)),
+                         dim3(Geo<64>::THREADS), 0, stream, a);
+  }
   return hipGetLastError();
 }
 

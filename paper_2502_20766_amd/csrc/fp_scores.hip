@@ -153,7 +153,9 @@ __global__ __launch_bounds__(kThreads) void rep_stats(SelectArgs a) {
   const float mu = (mm == -INFINITY) ? 0.f : mm;
   // fixed order: lower half's partial first
   const float lt = la * __builtin_amdgcn_exp2f(ma - mu) + lb * __builtin_amdgcn_exp2f(mb - mu);
-  if (lh == 0) a.chunk_stats[((int64_t)c * a.hq + h) * a.block + r] = make_float2(mm, lt);
+  // rows r >= block do not exist (block 64 uses two of the four waves' rows)
+  if (lh == 0 && r < a.block)
+    a.chunk_stats[((int64_t)c * a.hq + h) * a.block + r] = make_float2(mm, lt);
 }
 
 // Merge the chunk statistics of each representative row, in chunk order.

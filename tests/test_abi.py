@@ -67,7 +67,9 @@ def test_sizes(lib):
     (dict(hq=3, hkv=2), fpx.FP_ERR_INVALID_ARG),
     (dict(hq=0), fpx.FP_ERR_INVALID_ARG),
     (dict(d=96), fpx.FP_ERR_UNSUPPORTED),
-    (dict(block=64), fpx.FP_ERR_UNSUPPORTED),
+    (dict(block=32), fpx.FP_ERR_UNSUPPORTED),
+    (dict(block=64), fpx.FP_OK),
+    (dict(block=64, cu=(0, 8192 * 64 + 1)), fpx.FP_ERR_UNSUPPORTED),  # > 8192 blocks
     (dict(cu=(0, 100, 90)), fpx.FP_ERR_INVALID_ARG),      # non-monotone
     (dict(cu=(0, 100, 100)), fpx.FP_ERR_INVALID_ARG),     # empty sequence
     (dict(cu=(5, 100)), fpx.FP_ERR_INVALID_ARG),          # cu[0] != 0

@@ -256,3 +256,72 @@ def test_query_wise_selection_and_max_budget_vs_oracle(case):
     mx, mean = compare_outputs(layer, g["o"], g["masks"], rows_per_head=4)
     log(f"  output max_abs {mx:.3e} mean_abs {mean:.3e}")
     assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
+
+
+# ---------------------------------------------------------------- block 64
+
+B64_ATTN_CASES = [
+    # (name, seqlens, hq, hkv, d, mask density)
+    ("b64-ragged-varlen-d128", (300, 129, 1, 1000, 64, 65), 4, 2, 128, 0.4),
+    ("b64-gqa4-d64-n2048", (2048,), 8, 2, 64, 0.5),
+    ("b64-dense-d128-n1000", (1000,), 2, 1, 128, 1.0),
+]
+
+
+@pytest.mark.parametrize("case", B64_ATTN_CASES, ids=[c[0] for c in B64_ATTN_CASES])
+def test_block64_attention_on_oracle_masks(case):
+    name, seqlens, hq, hkv, d, dens = case
+    log(f"[b64 attn-oracle-masks] {name}")
+    fpx = _fpx()
+    kinds = tuple("vs" if h % 2 == 0 else "qa" for h in range(hq))
+    spec = synth.LayerSpec(name, seqlens, hq, hkv, d, 64, kinds, 8, 0.9, 0.1, 2, 4242)
+    layer = synth.make_layer(spec)
+    rng = np.random.default_rng(64)
+    masks = {}
+    for s_, n in enumerate(seqlens):
+        nb = -(-n // 64)
+        for h in range(hq):
+            m = np.tril(rng.random((nb, nb)) < dens)
+            m[np.arange(nb), 0] = True
+            m[np.arange(nb), np.arange(nb)] = True
+            masks[(s_, h)] = m
+    q, k, v = to_device(layer)
+    shape = fpx.Shape(layer.cu_seqlens, hq, hkv, d, 64)
+    idx = fpx.indices_from_masks(shape, masks, q.device)
+    o = fpx.sparse_attn(q, k, v, idx)
+    torch.cuda.synchronize()
+    mx, mean = compare_outputs(layer, o.float().cpu().numpy(), masks)
+    log(f"  max_abs {mx:.3e} mean_abs {mean:.3e}")
+    assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
+
+
+B64_SELECT_CASES = [
+    ("b64-tiny", synth.SPECS["tiny"].with_params(block=64)),
+    ("b64-mixed-8h-n8192", MIXED.with_params(block=64)),
+    ("b64-ragged-varlen", RAGGED.with_params(block=64)),
+    ("b64-glm-gqa16-n8192", GLM.with_params(block=64)),
+]
+
+
+@pytest.mark.parametrize("case", B64_SELECT_CASES, ids=[c[0] for c in B64_SELECT_CASES])
+def test_block64_select_and_attention_vs_oracle(case):
+    """The whole path at block size 64 (block sets exact up to the gamma band, outputs on
+    the device's lists)."""
+    fpx = _fpx()
+    name, spec = case
+    log(f"[b64 select+attn] {name} seqlens={spec.seqlens} hq={spec.hq} hkv={spec.hkv}")
+    layer = synth.make_layer(spec)
+    q, k, v = to_device(layer)
+    idx = fpx.select(q, k, layer.cu_seqlens, spec.gamma, spec.tau, spec.min_budget, block=64)
+    o = fpx.sparse_attn(q, k, v, idx)
+    torch.cuda.synchronize()
+    g = dict(masks=fpx.masks_from_indices(idx), pattern=idx.pattern.cpu().numpy(),
+             js=idx.js.cpu().numpy(), units=idx.units.cpu().numpy(),
+             o=o.float().cpu().numpy(), idx=idx)
+    check_lists_structure(idx, layer, spec.min_budget)
+    with Timer("oracle selection"):
+        st = compare_selection(layer, g, spec.gamma, spec.tau, spec.min_budget)
+    log(f"  {st}")
+    mx, mean = compare_outputs(layer, g["o"], g["masks"], rows_per_head=6)
+    log(f"  output max_abs {mx:.3e} mean_abs {mean:.3e}")
+    assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
