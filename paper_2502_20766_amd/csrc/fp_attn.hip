@@ -157,36 +157,18 @@ __device__ __forceinline__ void lds_write_i32(uint32_t addr, int v) {
   asm volatile("ds_write_b32 %0, %1" ::"v"(addr), "v"(v) : "memory");
 }
 
-// One 16-key step of V^T fragments: DB d-blocks x 2 key halves of ds_read_b64_tr_b16.
-// The loads and their lgkmcnt wait are one asm block, so the outputs are only defined
-// once the data has arrived; the compiler's own (conservative) wait for the in-flight
-// DMA of the next stage is thereby avoided.
+// One 16-key step of V^T fragments: DB d-blocks x 2 key halves of ds_read_b64_tr_b16
+// (through the compiler builtin, so the reads of one step are scheduled under the MFMAs
+// of the previous one with partial lgkmcnt waits).
 template <int DB, int OFF0, int OFF1>
 __device__ __forceinline__ void v_frags(const uint32_t (&addr)[DB], s16x4 (&lo)[DB],
                                         s16x4 (&hi)[DB]) {
-  if constexpr (DB == 4) {
-    asm volatile(
-        "ds_read_b64_tr_b16 %0, %8 offset:%12\n\t"
-        "ds_read_b64_tr_b16 %1, %8 offset:%13\n\t"
-        "ds_read_b64_tr_b16 %2, %9 offset:%12\n\t"
-        "ds_read_b64_tr_b16 %3, %9 offset:%13\n\t"
-        "ds_read_b64_tr_b16 %4, %10 offset:%12\n\t"
-        "ds_read_b64_tr_b16 %5, %10 offset:%13\n\t"
-        "ds_read_b64_tr_b16 %6, %11 offset:%12\n\t"
-        "ds_read_b64_tr_b16 %7, %11 offset:%13\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(lo[0]), "=&v"(hi[0]), "=&v"(lo[1]), "=&v"(hi[1]), "=&v"(lo[2]), "=&v"(hi[2]),
-          "=&v"(lo[3]), "=&v"(hi[3])
-        : "v"(addr[0]), "v"(addr[1]), "v"(addr[2]), "v"(addr[3]), "i"(OFF0), "i"(OFF1));
-  } else {
-    asm volatile(
-        "ds_read_b64_tr_b16 %0, %4 offset:%6\n\t"
-        "ds_read_b64_tr_b16 %1, %4 offset:%7\n\t"
-        "ds_read_b64_tr_b16 %2, %5 offset:%6\n\t"
-        "ds_read_b64_tr_b16 %3, %5 offset:%7\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(lo[0]), "=&v"(hi[0]), "=&v"(lo[1]), "=&v"(hi[1])
-        : "v"(addr[0]), "v"(addr[1]), "i"(OFF0), "i"(OFF1));
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    lo[db] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4 *)(uintptr_t)(addr[db] + OFF0));
+    hi[db] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4 *)(uintptr_t)(addr[db] + OFF1));
   }
 }
 
