@@ -31,6 +31,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
@@ -56,6 +57,20 @@ __device__ __forceinline__ float wave_pair_max(float x) {
 __device__ __forceinline__ float wave_pair_sum(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// acc + the sum of two 16-key steps' bf16 weights -- exactly the values the P V products
+// use -- two per v_dot2_f32_bf16 against (1, 1).
+__device__ __forceinline__ float sum_weights(const bf16x8 (&pf)[2], float acc) {
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bf16x2 pair = {pf[i][2 * e], pf[i][2 * e + 1]};
+      acc = __builtin_amdgcn_fdot2_f32_bf16(pair, one, acc, false);
+    }
+  return acc;
 }
 
 // Geometry of one stage in LDS (K and V both row-major [key][d], bf16).
@@ -463,7 +478,7 @@ void sparse_fa_fwd(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < DB; ++i) oacc[i] = f32x16{};
     float m_ref = -INFINITY;   // reference max (raw logit units) of this lane's row
-    float l_run = 0.f;          // this lane's share of the row sum (its 32 of 64 keys)
+    float l_run = 0.f;          // this lane's share of the row sum of the bf16 weights
     int J_cur = cur.J0;         // block of the stage being prefetched
     int J_pre = cur.J1;         // block after it
     // stage t covers keys J*128 + 64*(t&1) .. +63 of block J = list[t >> 1]; a row with no
@@ -576,12 +591,12 @@ void sparse_fa_fwd(AttnArgs a) {
       // sub-block 1 max; if the reference moved, sub-block 0's weights are recomputed
       if (update_max(mask_max(1))) weights0(p0);
       bf16x8 pf0[2];
-  #pragma unroll
+#pragma unroll
       for (int e = 0; e < 8; ++e) {
         pf0[0][e] = (__bf16)p0[e];
         pf0[1][e] = (__bf16)p0[8 + e];
-        l_run += p0[e] + p0[8 + e];
       }
+      l_run = sum_weights(pf0, l_run);
 
       {
         s16x4 vlo[DB], vhi[DB];
@@ -594,12 +609,12 @@ void sparse_fa_fwd(AttnArgs a) {
       bf16x8 pf1[2];
       {
         const float mc = (m_ref == -INFINITY) ? 0.f : m_ref * c;
-  #pragma unroll
+#pragma unroll
         for (int v = 0; v < 16; ++v) {
           const float p = __builtin_amdgcn_exp2f(fmaf(sacc[1][v], c, -mc));
           pf1[v >> 3][v & 7] = (__bf16)p;
-          l_run += p;
         }
+        l_run = sum_weights(pf1, l_run);
       }
       {
         s16x4 vlo[DB], vhi[DB];
@@ -619,8 +634,8 @@ void sparse_fa_fwd(AttnArgs a) {
       for (int e = 0; e < 8; ++e) {
         pf0[0][e] = (__bf16)p0[e];
         pf0[1][e] = (__bf16)p0[8 + e];
-        l_run += p0[e] + p0[8 + e];
       }
+      l_run = sum_weights(pf0, l_run);
       s16x4 vlo[DB], vhi[DB];
       v_frags<DB, 0 * 16 * S::RB, 0 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
       pv_step(pf0[0], vlo, vhi);
