@@ -106,6 +106,7 @@ size_t select_layout(const fp_shape *sh, const Dims &dm, char *base, fp::SelectA
   char *a_s = take(sizeof(float) * hq * dm.total_tokens);
   char *av_blk = take(sizeof(float) * hq * dm.nb_total);
   char *as_blk = take(sizeof(float) * hq * dm.nb_total);
+  char *vs_marks = take(4 * hq * dm.nb_total);
   char *flat = take(sizeof(float) * hq * dm.tri_total);
   char *sel = take(sizeof(fp::SelState) * problems);
   char *hist_cnt = take(sizeof(uint32_t) * problems * fp::kHistBuckets);
@@ -119,6 +120,7 @@ size_t select_layout(const fp_shape *sh, const Dims &dm, char *base, fp::SelectA
     a->a_s = (float *)a_s;
     a->av_blk = (float *)av_blk;
     a->as_blk = (float *)as_blk;
+    a->vs_marks = (uint8_t *)vs_marks;
     a->flat = (float *)flat;
     a->sel = (fp::SelState *)sel;
     a->hist_cnt = (uint32_t *)hist_cnt;

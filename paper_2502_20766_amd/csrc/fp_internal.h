@@ -48,6 +48,8 @@ struct SelectArgs {
   float *a_s;              // [Hq][T]
   float *av_blk;           // [Hq][NB] a_v summed per key block (block-pooled lines)
   float *as_blk;           // [Hq][NB] a_s summed per offset block
+  uint8_t *vs_marks;       // [Hq][NB][4] per key block / diagonal: column, diagonal (full
+                           // rows), diagonal (partial last row), diagonal + 1
   float *flat;             // [Hq][TRI]
   struct SelState *sel;    // [n_seq][Hq][2]
   uint32_t *hist_cnt;      // [n_seq][Hq][2][kHistBuckets]

@@ -86,6 +86,13 @@ __global__ void sel_init(SelectArgs a) {
     a.hist_cnt[(int64_t)p * kHistBuckets + b] = 0u;
     a.hist_mass[(int64_t)p * kHistBuckets + b] = 0ull;
   }
+  if ((p & 1) == 0) {                     // clear the line marks of this (sequence, head)
+    const int sh = p >> 1, s = sh / a.hq, h = sh % a.hq;
+    const int nb = a.st.nb_off[s + 1] - a.st.nb_off[s];
+    uint32_t *mk = reinterpret_cast<uint32_t *>(a.vs_marks) +
+                   (int64_t)h * a.nb_total + a.st.nb_off[s];
+    for (int i = threadIdx.x; i < nb; i += blockDim.x) mk[i] = 0u;
+  }
   if (threadIdx.x == 0) {
     const Problem pr = problem_of(a, p);
     SelState S = {};
@@ -268,6 +275,58 @@ __global__ __launch_bounds__(1024) void sel_tie(SelectArgs a) {
 
 // ---------------------------------------------------------------- conversion to lists
 
+// Vertical-slash heads: mark, per key block / block diagonal, what the selected lines
+// reach (vertical j: column floor(j/b); slash o = D*b + t: diagonal D in full query blocks,
+// diagonal D in the partial last query block when t < its rows, diagonal D+1 when t > 0).
+// One workgroup per (sequence, head, slice of kMarkSlice lines); the stores only ever
+// write 1, so their order does not matter.
+constexpr int kMarkSlice = 8192;
+
+__global__ __launch_bounds__(256) void vs_marks(SelectArgs a) {
+  const int s = blockIdx.x / a.hq, h = blockIdx.x % a.hq;
+  if (a.pattern[s * a.hq + h] != FP_PATTERN_VERTICAL_SLASH) return;
+  const int tok0 = a.st.cu[s];
+  const int n = a.st.cu[s + 1] - tok0;
+  const int b = a.block;
+  const int nb = a.st.nb_off[s + 1] - a.st.nb_off[s];
+  const int last_rows = n - (nb - 1) * b;
+  const int p0 = (s * a.hq + h) * 2;
+  const SelState S0 = a.sel[p0];
+  const SelState S1 = a.sel[p0 + 1];
+  uint8_t *mk = a.vs_marks + 4 * ((int64_t)h * a.nb_total + a.st.nb_off[s]);
+  if (a.vs_granularity == 1) {
+    // a selected unit selects all its lines: key block J is a column; offset block D
+    // holds o = D*b (t = 0: diagonal D in every row) and, when it has more than one
+    // offset, o = D*b + t with t > 0 (diagonal D + 1)
+    const int u = blockIdx.y * blockDim.x + threadIdx.x;
+    if (u >= nb) return;
+    const float *avb = a.av_blk + (int64_t)h * a.nb_total + a.st.nb_off[s];
+    const float *asb = a.as_blk + (int64_t)h * a.nb_total + a.st.nb_off[s];
+    if (is_selected(S0, avb[u], u)) mk[4 * u + 0] = 1;
+    if (is_selected(S1, asb[u], u)) {
+      mk[4 * u + 1] = 1;
+      mk[4 * u + 2] = 1;
+      if (n - u * b > 1 && u + 1 < nb) mk[4 * (u + 1) + 3] = 1;
+    }
+    return;
+  }
+  const float *av = a.a_v + (int64_t)h * a.total_tokens + tok0;
+  const float *as = a.a_s + (int64_t)h * a.total_tokens + tok0;
+  const int j0 = blockIdx.y * kMarkSlice;
+  const int j1 = min(j0 + kMarkSlice, n);
+  for (int j = j0 + threadIdx.x; j < j1; j += blockDim.x) {
+    if (is_selected(S0, av[j], j)) mk[4 * (j / b) + 0] = 1;
+    if (is_selected(S1, as[j], j)) {
+      const int dl = j / b, t = j % b;
+      mk[4 * dl + 1] = 1;
+      if (t < last_rows) mk[4 * dl + 2] = 1;
+      if (t > 0 && dl + 1 < nb) mk[4 * (dl + 1) + 3] = 1;
+    }
+  }
+}
+
+// Lists of one (sequence, head): grid (sequence * head, row slice); wave w of slice r
+// converts rows I = 16 r + w + 16 R k.
 __global__ __launch_bounds__(1024) void convert_tiles(SelectArgs a) {
   __shared__ uint8_t colsel[kMaxNb];
   __shared__ uint8_t d0[kMaxNb];
@@ -275,63 +334,45 @@ __global__ __launch_bounds__(1024) void convert_tiles(SelectArgs a) {
   __shared__ uint8_t d1[kMaxNb + 1];
   __shared__ int added[16][FP_MAX_MIN_BUDGET];
   const int s = blockIdx.x / a.hq, h = blockIdx.x % a.hq;
+  const int slice = blockIdx.y, n_slices = gridDim.y;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int tok0 = a.st.cu[s];
   const int n = a.st.cu[s + 1] - tok0;
   const int b = a.block;
   const int nb = a.st.nb_off[s + 1] - a.st.nb_off[s];
-  const int last_rows = n - (nb - 1) * b;            // rows of the last query block
   const int pat = a.pattern[s * a.hq + h];
   const bool vs = pat == FP_PATTERN_VERTICAL_SLASH;
   const int p0 = (s * a.hq + h) * 2;
   const SelState S0 = a.sel[p0];
   const SelState S1 = a.sel[p0 + 1];
   const float *flat = a.flat + (int64_t)h * a.tri_total + a.st.tri_off[s];
+  (void)tok0;
+  (void)n;
+  if (slice * 16 >= nb) return;                 // no row of this (sequence, head) here
 
   if (vs) {
-    for (int i = tid; i <= nb; i += blockDim.x) {
-      if (i < nb) { colsel[i] = 0; d0[i] = 0; d0p[i] = 0; }
-      d1[i] = 0;
+    const uint32_t *mk = reinterpret_cast<const uint32_t *>(a.vs_marks) +
+                         (int64_t)h * a.nb_total + a.st.nb_off[s];
+    for (int i = tid; i < nb; i += blockDim.x) {
+      const uint32_t m4 = mk[i];
+      colsel[i] = m4 & 0xFF;
+      d0[i] = (m4 >> 8) & 0xFF;
+      d0p[i] = (m4 >> 16) & 0xFF;
+      d1[i] = m4 >> 24;
     }
-    __syncthreads();
-    if (a.vs_granularity == 1) {
-      // a selected unit selects all its lines: key block J is a column; offset block D
-      // holds o = D*b (t = 0: diagonal D in every row) and, when it has more than one
-      // offset, o = D*b + t with t > 0 (diagonal D + 1)
-      const float *avb = a.av_blk + (int64_t)h * a.nb_total + a.st.nb_off[s];
-      const float *asb = a.as_blk + (int64_t)h * a.nb_total + a.st.nb_off[s];
-      for (int u = tid; u < nb; u += blockDim.x) {
-        if (is_selected(S0, avb[u], u)) colsel[u] = 1;
-        if (is_selected(S1, asb[u], u)) {
-          d0[u] = 1;
-          d0p[u] = 1;
-          if (n - u * b > 1) d1[u + 1] = 1;
-        }
-      }
-    } else {
-      const float *av = a.a_v + (int64_t)h * a.total_tokens + tok0;
-      const float *as = a.a_s + (int64_t)h * a.total_tokens + tok0;
-      for (int j = tid; j < n; j += blockDim.x) {
-        if (is_selected(S0, av[j], j)) colsel[j / b] = 1;
-        if (is_selected(S1, as[j], j)) {
-          const int dl = j / b, t = j % b;
-          d0[dl] = 1;
-          if (t < last_rows) d0p[dl] = 1;
-          if (t > 0) d1[dl + 1] = 1;
-        }
-      }
-    }
+    if (tid == 0) d1[nb] = 0;
     __syncthreads();
   }
-  if (tid == 0) {
+  if (tid == 0 && slice == 0) {
     // per-query-block selection accumulates its K over the rows (qa_rows, launched next)
     a.units[(s * a.hq + h) * 2 + 0] = (!vs && a.qa_mode == 1) ? 0 : S0.k;
     a.units[(s * a.hq + h) * 2 + 1] = vs ? S1.k : 0;
   }
   if (!vs && (a.qa_mode == 1 || a.max_budget > 0)) return;   // rows written by qa_rows
+  const int last_rows = n - (nb - 1) * b;            // rows of the last query block
 
   const int m = a.min_budget;
-  for (int I = w; I < nb; I += 16) {
+  for (int I = slice * 16 + w; I < nb; I += 16 * n_slices) {
     const bool row_full = (I < nb - 1) || (last_rows == b);
     const int64_t tri_row = (int64_t)I * (I + 1) / 2;
     auto sel = [&](int J) -> bool {
@@ -670,7 +711,18 @@ hipError_t launch_select_pipeline(const SelectArgs &a, hipStream_t stream) {
   hipLaunchKernelGGL(sel_hist<2>, dim3(slices, problems), dim3(256), 0, stream, a);
   hipLaunchKernelGGL(sel_scan<2>, dim3(problems), dim3(256), 0, stream, a);
   hipLaunchKernelGGL(sel_tie, dim3(problems), dim3(1024), 0, stream, a);
-  hipLaunchKernelGGL(convert_tiles, dim3(a.st.n_seq * a.hq), dim3(1024), 0, stream, a);
+  {
+    int max_n = 0;
+    for (int s = 0; s < a.st.n_seq; ++s) max_n = max(max_n, a.st.cu[s + 1] - a.st.cu[s]);
+    const int mark_slices = a.vs_granularity == 1 ? (a.st.max_nb + 255) / 256
+                                                  : (max_n + kMarkSlice - 1) / kMarkSlice;
+    hipLaunchKernelGGL(vs_marks, dim3(a.st.n_seq * a.hq, mark_slices), dim3(256), 0, stream, a);
+    // row slices: about two workgroups per CU over all (sequence, head) pairs
+    const int pairs = a.st.n_seq * a.hq;
+    int slices = (512 + pairs - 1) / pairs;
+    slices = max(1, min(slices, (a.st.max_nb + 15) / 16));
+    hipLaunchKernelGGL(convert_tiles, dim3(pairs, slices), dim3(1024), 0, stream, a);
+  }
   if (a.qa_mode == 1 || a.max_budget > 0) {
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return launch_qa_rows(a, stream);
