@@ -44,22 +44,33 @@ __device__ __forceinline__ int k_swz(int chunk, int key) {
   else return chunk ^ ((key >> 1) & 7);
 }
 
-// Stage keys [kt, kt + KT) of KV head g (rows past n are zero) into LDS, swizzled.
+// Keys [kt, kt + KT) of KV head g (rows past n are zero), staged through registers: the
+// next tile is loaded while the current one is in use, then stored to LDS swizzled.
 template <int D>
-__device__ __forceinline__ void stage_k_tile(uint16_t *Ks, const uint16_t *kbase,
-                                             int64_t kv_row, int kt, int n, int tid) {
-  constexpr int KCH = D / 8;
+struct KTile {
+  static constexpr int KCH = D / 8;                     // 16-byte chunks per key
+  static constexpr int NIT = KT * KCH / kThreads;       // chunks per thread
+  uint4 v[NIT];
+  __device__ __forceinline__ void load(const uint16_t *kbase, int64_t kv_row, int kt, int n,
+                                       int tid) {
 #pragma unroll
-  for (int it = 0; it < KT * KCH / kThreads; ++it) {
-    const int c = it * kThreads + tid;
-    const int key = c / KCH;
-    const int ch = c % KCH;
-    const int j = kt + key;
-    uint4 val = *reinterpret_cast<const uint4 *>(kbase + (int64_t)min(j, n - 1) * kv_row + ch * 8);
-    if (j >= n) val = make_uint4(0, 0, 0, 0);
-    *reinterpret_cast<uint4 *>(Ks + key * D + k_swz<D>(ch, key) * 8) = val;
+    for (int it = 0; it < NIT; ++it) {
+      const int c = it * kThreads + tid;
+      const int j = kt + c / KCH;
+      v[it] = *reinterpret_cast<const uint4 *>(kbase + (int64_t)min(j, n - 1) * kv_row +
+                                               (c % KCH) * 8);
+      if (j >= n) v[it] = make_uint4(0, 0, 0, 0);
+    }
   }
-}
+  __device__ __forceinline__ void store(uint16_t *Ks, int tid) const {
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const int c = it * kThreads + tid;
+      const int key = c / KCH;
+      *reinterpret_cast<uint4 *>(Ks + key * D + k_swz<D>(c % KCH, key) * 8) = v[it];
+    }
+  }
+};
 
 // S^T for 64 keys x the wave's 32 query rows: two 32x32 MFMA blocks.
 template <int D>
@@ -117,10 +128,13 @@ __global__ __launch_bounds__(kThreads) void rep_stats(SelectArgs a) {
   bf16x8 qf[D / 16];
   load_qhat<D>(a, tok0, n, h, r, lh, qf);
   float m = -INFINITY, l = 0.f;
+  KTile<D> tile;
+  tile.load(kbase, kv_row, c0, n, tid);
   for (int kt = c0; kt < c1; kt += KT) {
     __syncthreads();
-    stage_k_tile<D>(Ks, kbase, kv_row, kt, n, tid);
+    tile.store(Ks, tid);
     __syncthreads();
+    if (kt + KT < c1) tile.load(kbase, kv_row, kt + KT, n, tid);   // overlaps this tile
     f32x16 sacc[2];
     tile_scores<D>(Ks, qf, lr, lh, sacc);
     float mt = -INFINITY;
@@ -209,10 +223,13 @@ __global__ __launch_bounds__(kThreads) void rep_lines(SelectArgs a) {
 
   // keys [c0 - 128, c0) are recomputed for the diagonals owned by this chunk
   const int kstart = max(c0 - 128, 0);
+  KTile<D> tile;
+  tile.load(kbase, kv_row, kstart, n, tid);
   for (int kt = kstart; kt < c1; kt += KT) {
     __syncthreads();
-    stage_k_tile<D>(Ks, kbase, kv_row, kt, n, tid);
+    tile.store(Ks, tid);
     __syncthreads();
+    if (kt + KT < c1) tile.load(kbase, kv_row, kt + KT, n, tid);   // overlaps this tile
     f32x16 sacc[2];
     tile_scores<D>(Ks, qf, lr, lh, sacc);
 #pragma unroll
