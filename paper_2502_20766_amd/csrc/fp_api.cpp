@@ -129,9 +129,11 @@ size_t select_layout(const fp_shape *sh, const Dims &dm, char *base, fp::SelectA
   return off;
 }
 
-// attention workspace: ordered item records [Hq][NB] int4, then 8 queue counters
+// attention workspace: ordered item records [Hq][NB] int4, 8 queue counters, then the V^T
+// tiles [Hkv][NB][block * d] bf16
 size_t attn_layout(const fp_shape *sh, const Dims &dm) {
-  return align_up(16 * dm.nb_total * sh->num_q_heads) + align_up(8 * sizeof(int32_t));
+  return align_up(16 * dm.nb_total * sh->num_q_heads) + align_up(8 * sizeof(int32_t)) +
+         align_up(2 * (size_t)dm.nb_total * sh->num_kv_heads * sh->block * sh->head_dim);
 }
 
 fp_status hip_fail(hipError_t e, const char *what) {
@@ -265,6 +267,7 @@ fp_status fp_sparse_attn(const fp_shape *shape, const void *q, const void *k, co
   a.scale_log2 = scale * 1.4426950408889634f;
   a.items = (int4 *)ws;
   a.queue = (int32_t *)((char *)ws + align_up(16 * dm.nb_total * shape->num_q_heads));
+  a.vt = (uint16_t *)((char *)a.queue + align_up(8 * sizeof(int32_t)));
   hipError_t e = fp::launch_sparse_attn(a, (hipStream_t)stream);
   return e == hipSuccess ? FP_OK : hip_fail(e, "fp_sparse_attn");
 }

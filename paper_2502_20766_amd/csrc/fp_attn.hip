@@ -5,19 +5,20 @@
 // S is given at block granularity: for every (sequence, query head, query block I) an
 // ascending list of key blocks J <= I.
 //
-// One workgroup = one (sequence, query head, query block) row of 128 queries; 4 waves of
-// 32 query rows each.  Per selected key block:
-//   * K tile [128 keys][d] is staged in LDS row-major with a 16-byte-chunk XOR swizzle;
-//   * V tile is staged transposed, Vt[d][128 keys], with an 8-byte-unit XOR swizzle, so
-//     that both the K fragment (ds_read_b128) and the V^T fragment (2 x ds_read_b64) are
-//     bank-conflict free;
+// One workgroup = one (sequence, query head, query block) row of B queries; B/32 waves of
+// 32 query rows each.  Per selected key block, in stages of B/2 keys:
+//   * K tile [keys][d] is staged in LDS row-major with a 16-byte-chunk XOR swizzle;
+//   * V is transposed once per call (stage_v_transposed) into 16-key steps of V^T,
+//     [step][d][16 keys], already in the swizzled LDS order, so its stage copy is linear
+//     and each V^T fragment is one conflict-free ds_read_b128;
 //   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (Q^T fragments live in registers), so each
-//     lane owns one query row and 64 of the 128 keys: the row max needs one lane swap;
+//     lane owns one query row and half of the stage's keys: the row max needs one lane
+//     swap.  K rows are read with bits 2 and 3 of the row index swapped, which makes the
+//     keys a lane holds in S^T exactly the 8 consecutive keys its P^T B-operand needs;
 //   * online softmax in the log2 domain (exp2 with log2(e) folded into the scale), the
 //     O rescale skipped when no row of the wave sees a new maximum;
-//   * O^T += V^T P^T on the same MFMA: P^T is already in B-operand layout (the key order
-//     inside each 16-key step is permuted identically on both operands), and O^T keeps
-//     one query row per lane, so the rescale by exp2(m_old - m_new) is per lane.
+//   * O^T += V^T P^T on the same MFMA, and O^T keeps one query row per lane, so the
+//     rescale by exp2(m_old - m_new) is per lane.
 // A persistent grid walks each KV group's (sequence, query head, query block) items in a
 // locality order (longest lists first in buckets, lists that start alike adjacent), every
 // group served by the same XCD(s), so that items running together share K/V tiles in L2.
@@ -73,7 +74,8 @@ __device__ __forceinline__ float sum_weights(const bf16x8 (&pf)[2], float acc) {
   return acc;
 }
 
-// Geometry of one stage in LDS (K and V both row-major [key][d], bf16).
+// Geometry of one stage in LDS: K row-major [key][d], V^T as [16-key step][d][16 keys]
+// (bf16, 16-byte units placed by vt_unit).
 template <int D, int B>
 struct Stage {
   static constexpr int RB = 2 * D;                 // bytes per key row
@@ -91,16 +93,18 @@ __device__ __forceinline__ int swz_k(int y, int r) {
   if constexpr (D == 128) return y ^ (r & 15);
   else return y ^ ((r >> 1) & 7);
 }
-// V: the 4 consecutive rows x 4 chunks read by one half-wave transposing load are distinct.
-template <int D>
-__device__ __forceinline__ int swz_v(int y, int r) {
-  if constexpr (D == 128) return y ^ ((r & 3) << 2);
-  else return y ^ (((r >> 1) & 1) << 2);
+// V^T: 16-byte unit of (head dim d, key half lh) inside one 16-key step of 2 d units per d.
+// The 16 lanes that read one step at the same lh (d = d0 .. d0 + 15) land in 16 distinct
+// 16-byte bank groups, and so do each 8 of them; the placement is additive in d / 32 and
+// in the step, so a lane's reads differ only by immediate offsets.
+__device__ __forceinline__ int vt_unit(int d, int lh) {
+  return 16 * (d >> 3) + 8 * (lh ^ ((d >> 3) & 1)) + (d & 7);
 }
 
 // Per-lane byte offsets of the DMA slots of one stage, relative to the stage's first key
-// row: slot i of wave w covers LDS bytes [(WAVES i + w) * 1024, +1024), lane l fills 16
-// bytes of tile row r with the logical chunk whose swizzled position is the lane's slot.
+// row (K) or first byte (V^T): slot i of wave w covers LDS bytes [(WAVES i + w) * 1024,
+// +1024); for K lane l fills 16 bytes of tile row r with the logical chunk whose swizzled
+// position is the lane's slot, for V^T (stored in LDS order) the copy is linear.
 template <int D, int B>
 struct DmaOffsets {
   uint32_t k[Stage<D, B>::DMA_PER_WAVE];
@@ -113,10 +117,11 @@ __device__ __forceinline__ DmaOffsets<D, B> dma_offsets(uint32_t row_bytes, int 
   DmaOffsets<D, B> o;
 #pragma unroll
   for (int i = 0; i < S::DMA_PER_WAVE; ++i) {
-    const int r = (i * Geo<B>::WAVES + w) * S::RPI + lane / S::CPR;
+    const int q = i * Geo<B>::WAVES + w;
+    const int r = q * S::RPI + lane / S::CPR;
     const int phys = lane % S::CPR;
     o.k[i] = r * row_bytes + swz_k<D>(phys, r) * 16;
-    o.v[i] = r * row_bytes + swz_v<D>(phys, r) * 16;
+    o.v[i] = q * 1024 + lane * 16;
   }
   return o;
 }
@@ -134,17 +139,18 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void *base,
                                            0x00020000);
 }
 
-// Issue the DMA of one stage: keys k0 .. k0+KEYS-1 of the sequence through buffer
-// descriptors whose range ends at the last valid key row, so rows past the sequence end
-// read as zeros (and are masked by the caller).
+// Issue the DMA of one stage: keys k0 .. k0+KEYS-1 of the sequence, K through a buffer
+// descriptor whose range ends at the last valid key row (rows past the sequence end read
+// as zeros and are masked by the caller), V^T as the stage's contiguous tile (zero past
+// the sequence end).
 template <int D, int B>
 __device__ __forceinline__ void stage_dma(uint8_t *ks, uint8_t *vs, const uint16_t *kbase,
-                                          const uint16_t *vbase, int64_t kv_row, int k0,
+                                          const uint16_t *vt_tile, int64_t kv_row, int k0,
                                           int kvalid, const DmaOffsets<D, B> &off) {
   using S = Stage<D, B>;
   const int nrec = (kvalid - 1) * (int)kv_row * 2 + 2 * D;
   const __amdgpu_buffer_rsrc_t rk = uniform_rsrc(kbase + (int64_t)k0 * kv_row, nrec);
-  const __amdgpu_buffer_rsrc_t rv = uniform_rsrc(vbase + (int64_t)k0 * kv_row, nrec);
+  const __amdgpu_buffer_rsrc_t rv = uniform_rsrc(vt_tile, S::BYTES);
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
   for (int i = 0; i < S::DMA_PER_WAVE; ++i) {
@@ -172,25 +178,11 @@ __device__ __forceinline__ void lds_write_i32(uint32_t addr, int v) {
   asm volatile("ds_write_b32 %0, %1" ::"v"(addr), "v"(v) : "memory");
 }
 
-// One 16-key step of V^T fragments: DB d-blocks x 2 key halves of ds_read_b64_tr_b16
-// (through the compiler builtin, so the reads of one step are scheduled under the MFMAs
-// of the previous one with partial lgkmcnt waits).
-template <int DB, int OFF0, int OFF1>
-__device__ __forceinline__ void v_frags(const uint32_t (&addr)[DB], s16x4 (&lo)[DB],
-                                        s16x4 (&hi)[DB]) {
-#pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    lo[db] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (__attribute__((address_space(3))) s16x4 *)(uintptr_t)(addr[db] + OFF0));
-    hi[db] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (__attribute__((address_space(3))) s16x4 *)(uintptr_t)(addr[db] + OFF1));
-  }
-}
-
 // One unit of work: the 128 queries of (sequence s, query head h, query block I).
 struct Row {
   int valid;
   int I, h, g, cnt, tok0, n;
+  int nb0;                        // global index of the sequence's first key block
   int J0, J1;                     // first two listed key blocks (-1 if absent)
   const __attribute__((address_space(4))) int32_t *list;
 };
@@ -251,6 +243,7 @@ __device__ __forceinline__ Row uniform_row(const Row &r) {
   u.cnt = __builtin_amdgcn_readfirstlane(r.cnt);
   u.tok0 = __builtin_amdgcn_readfirstlane(r.tok0);
   u.n = __builtin_amdgcn_readfirstlane(r.n);
+  u.nb0 = __builtin_amdgcn_readfirstlane(r.nb0);
   u.J0 = __builtin_amdgcn_readfirstlane(r.J0);
   u.J1 = __builtin_amdgcn_readfirstlane(r.J1);
   const uint64_t p = (uint64_t)(uintptr_t)r.list;
@@ -313,6 +306,7 @@ void sparse_fa_fwd(AttnArgs a) {
     r.I = packed & 0x1FFF;
     r.tok0 = a.st.cu[s];
     r.n = a.st.cu[s + 1] - r.tok0;
+    r.nb0 = a.st.nb_off[s];
     r.cnt = cnt;
     r.J0 = j0;
     r.J1 = j1;
@@ -423,27 +417,24 @@ void sparse_fa_fwd(AttnArgs a) {
   };
 
   const DmaOffsets<D, B> doff = dma_offsets<D, B>((uint32_t)(kv_row * 2), w, lane);
-  // per-lane V^T fragment addresses (relative to a V stage), one per d-block
-  uint32_t vaddr_rel[DB];
-  {
-    const int r_l = 4 * (g16 >> 1) + (i16 >> 2);       // row within a 16-key step
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const int dcol = 32 * db + 16 * (g16 & 1) + 4 * (i16 & 3);
-      vaddr_rel[db] = r_l * S::RB + swz_v<D>(dcol >> 3, r_l) * 16 + (dcol & 7) * 2;
-    }
-  }
+  // per-lane V^T fragment address (relative to a V^T stage) of d-block 0, step 0: d-block
+  // db adds 1 KB, step t adds 32 D bytes
+  const uint32_t vaddr_rel = 16 * vt_unit(lr, lh);
   // per-lane K fragment addresses (relative to a K stage) of sub-block 0; sub-block 1 is
-  // 32 rows further (the swizzles repeat every 32 rows)
+  // 32 rows further (the swizzles repeat every 32 rows).  MFMA row lr reads key row
+  // kr = lr with bits 2 and 3 swapped, so that S^T element v of lane (lr, lh) is key
+  // 16 (v / 8) + 8 lh + v % 8 of the sub-block.
+  const int kr = (lr & ~12) | ((lr >> 1) & 4) | ((lr << 1) & 8);
   uint32_t kaddr_rel[KS];
 #pragma unroll
-  for (int k = 0; k < KS; ++k) kaddr_rel[k] = lr * S::RB + swz_k<D>(2 * k + lh, lr) * 16;
+  for (int k = 0; k < KS; ++k) kaddr_rel[k] = kr * S::RB + swz_k<D>(2 * k + lh, kr) * 16;
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
   auto issue = [&](const Row &r, int k0, int into) {
     const uint16_t *kb = a.k + (int64_t)r.tok0 * kv_row + (int64_t)r.g * D;
-    const uint16_t *vbp = a.v + (int64_t)r.tok0 * kv_row + (int64_t)r.g * D;
+    const int jb = r.nb0 + (int)((uint32_t)k0 / B), koff = (int)((uint32_t)k0 % B);
+    const uint16_t *vt = a.vt + ((int64_t)(r.g * a.nb_total + jb) * B + koff) * D;
     uint8_t *dst = lds + into * 2 * S::BYTES;
-    stage_dma<D, B>(dst, dst + S::BYTES, kb, vbp, kv_row, k0, min(S::KEYS, r.n - k0), doff);
+    stage_dma<D, B>(dst, dst + S::BYTES, kb, vt, kv_row, k0, min(S::KEYS, r.n - k0), doff);
   };
 
   if (!cur.valid) {                       // this XCD's queue had no first item: take one
@@ -532,7 +523,7 @@ void sparse_fa_fwd(AttnArgs a) {
       if (diag) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int key = kq + b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
+          const int key = kq + b2 * 32 + 16 * (v >> 3) + 8 * lh + (v & 7);
           if (key > qrow) sacc[b2][v] = -INFINITY;
         }
       }
@@ -561,18 +552,17 @@ void sparse_fa_fwd(AttnArgs a) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) p0[v] = __builtin_amdgcn_exp2f(fmaf(sacc[0][v], c, -mc));
     };
-    // ---- O^T += V^T P^T, 16 keys per step; V^T fragments by transposing loads
-    uint32_t va[DB];
+    // ---- O^T += V^T P^T, 16 keys per step; one ds_read_b128 per V^T fragment
+    const uint8_t *vs = lds + ((buf ^ 1) * 2 + 1) * S::BYTES + vaddr_rel;
+    auto pv_step = [&](auto tc, const bf16x8 &pf) {
+      constexpr int t = decltype(tc)::value;
+      bf16x8 vf[DB];
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
-      va[db] = lds_base + ((buf ^ 1) * 2 + 1) * S::BYTES + vaddr_rel[db];
-    auto pv_step = [&](const bf16x8 &pf, s16x4 (&vlo)[DB], s16x4 (&vhi)[DB]) {
+      for (int db = 0; db < DB; ++db)
+        vf[db] = *reinterpret_cast<const bf16x8 *>(vs + db * 1024 + t * 32 * D);
 #pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        const s16x8 vv = __builtin_shufflevector(vlo[db], vhi[db], 0, 1, 2, 3, 4, 5, 6, 7);
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pf,
-                                                           oacc[db], 0, 0, 0);
-      }
+      for (int db = 0; db < DB; ++db)
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db], pf, oacc[db], 0, 0, 0);
     };
     if constexpr (Geo<B>::SUB == 2) {
       // sub-block 0 scores and running max
@@ -598,13 +588,8 @@ void sparse_fa_fwd(AttnArgs a) {
       }
       l_run = sum_weights(pf0, l_run);
 
-      {
-        s16x4 vlo[DB], vhi[DB];
-        v_frags<DB, 0 * 16 * S::RB, 0 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
-        pv_step(pf0[0], vlo, vhi);
-        v_frags<DB, 1 * 16 * S::RB, 1 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
-        pv_step(pf0[1], vlo, vhi);
-      }
+      pv_step(std::integral_constant<int, 0>{}, pf0[0]);
+      pv_step(std::integral_constant<int, 1>{}, pf0[1]);
       // sub-block 1 weights (VALU) overlap the PV MFMAs of sub-block 0
       bf16x8 pf1[2];
       {
@@ -616,13 +601,8 @@ void sparse_fa_fwd(AttnArgs a) {
         }
         l_run = sum_weights(pf1, l_run);
       }
-      {
-        s16x4 vlo[DB], vhi[DB];
-        v_frags<DB, 2 * 16 * S::RB, 2 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
-        pv_step(pf1[0], vlo, vhi);
-        v_frags<DB, 3 * 16 * S::RB, 3 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
-        pv_step(pf1[1], vlo, vhi);
-      }
+      pv_step(std::integral_constant<int, 2>{}, pf1[0]);
+      pv_step(std::integral_constant<int, 3>{}, pf1[1]);
     } else {
       // one 32-key sub-block per stage (block 64)
       qk_block(std::integral_constant<int, 0>{});
@@ -636,11 +616,8 @@ void sparse_fa_fwd(AttnArgs a) {
         pf0[1][e] = (__bf16)p0[8 + e];
       }
       l_run = sum_weights(pf0, l_run);
-      s16x4 vlo[DB], vhi[DB];
-      v_frags<DB, 0 * 16 * S::RB, 0 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
-      pv_step(pf0[0], vlo, vhi);
-      v_frags<DB, 1 * 16 * S::RB, 1 * 16 * S::RB + 8 * S::RB>(va, vlo, vhi);
-      pv_step(pf0[1], vlo, vhi);
+      pv_step(std::integral_constant<int, 0>{}, pf0[0]);
+      pv_step(std::integral_constant<int, 1>{}, pf0[1]);
     }
     }
 
@@ -684,6 +661,45 @@ __device__ __forceinline__ int seq_of_row(const SeqTable &st, int r) {
     if (st.nb_off[mid] <= r) lo = mid; else hi = mid;
   }
   return lo;
+}
+
+// V^T tiles for the attention stages: for KV head h and global key block gb (B keys of
+// one sequence), the B x D slice of V is written as B/16 steps of [d][16 keys], each
+// 16-byte unit (8 keys of one d) at vt_unit(d, key half) of its step -- the order the
+// attention kernel keeps in LDS.  Keys past the sequence end are zero.  Grid: (NB, Hkv).
+template <int D, int B>
+__global__ __launch_bounds__(256) void stage_v_transposed(SeqTable st, const uint16_t *v, int hkv,
+                                                          int nb_total, uint16_t *vt) {
+  constexpr int UPR = D / 8;               // 16-byte units per key row of the slice
+  __shared__ uint4 tile[B * UPR];          // [key][d] with the unit index XOR (key % UPR)
+  const int gb = blockIdx.x, h = blockIdx.y;
+  const int s = seq_of_row(st, gb);
+  const int tok = st.cu[s] + (gb - st.nb_off[s]) * B;
+  const int nvalid = min(B, st.cu[s + 1] - tok);
+  for (int u = threadIdx.x; u < B * UPR; u += blockDim.x) {
+    const int key = u / UPR, c = u % UPR;
+    uint4 val = make_uint4(0, 0, 0, 0);
+    if (key < nvalid)
+      val = *reinterpret_cast<const uint4 *>(v + ((int64_t)(tok + key) * hkv + h) * D + 8 * c);
+    tile[key * UPR + (c ^ (key % UPR))] = val;
+  }
+  __syncthreads();
+  const uint16_t *t16 = reinterpret_cast<const uint16_t *>(tile);
+  uint4 *out = reinterpret_cast<uint4 *>(vt + ((int64_t)h * nb_total + gb) * B * D);
+  for (int p = threadIdx.x; p < B * UPR; p += blockDim.x) {
+    const int step = p / (2 * D), w = p % (2 * D);
+    const int d = 8 * (w >> 4) + (w & 7);
+    const int lh = ((w >> 3) & 1) ^ ((w >> 4) & 1);
+    uint32_t word[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int k0 = 16 * step + 8 * lh + 2 * e;
+      const uint32_t lo = t16[(k0 * UPR + ((d >> 3) ^ (k0 % UPR))) * 8 + (d & 7)];
+      const uint32_t hi = t16[((k0 + 1) * UPR + ((d >> 3) ^ ((k0 + 1) % UPR))) * 8 + (d & 7)];
+      word[e] = lo | (hi << 16);
+    }
+    out[p] = make_uint4(word[0], word[1], word[2], word[3]);
+  }
 }
 
 // Plain item order, used when a group has too many items for the in-LDS sort: rows by query
@@ -797,6 +813,22 @@ hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t stream) {
     hipLaunchKernelGGL(build_item_order_plain, dim3((a.nb_total + 255) / 256), dim3(256), 0,
                        stream, a.st, a.kb_idx, a.kb_cnt, a.hq, a.hkv, a.tri_total, a.items,
                        a.queue);
+  const dim3 vt_grid(a.nb_total, a.hkv);
+  if (a.block == 128) {
+    if (a.d == 128)
+      hipLaunchKernelGGL((stage_v_transposed<128, 128>), vt_grid, dim3(256), 0, stream, a.st, a.v,
+                         a.hkv, a.nb_total, a.vt);
+    else
+      hipLaunchKernelGGL((stage_v_transposed<64, 128>), vt_grid, dim3(256), 0, stream, a.st, a.v,
+                         a.hkv, a.nb_total, a.vt);
+  } else {
+    if (a.d == 128)
+      hipLaunchKernelGGL((stage_v_transposed<128, 64>), vt_grid, dim3(256), 0, stream, a.st, a.v,
+                         a.hkv, a.nb_total, a.vt);
+    else
+      hipLaunchKernelGGL((stage_v_transposed<64, 64>), vt_grid, dim3(256), 0, stream, a.st, a.v,
+                         a.hkv, a.nb_total, a.vt);
+  }
   // Persistent grid: resident workgroups for two waves per SIMD (a multiple of 8, one
   // share per XCD), no more than there are items.
   static int cus = 0;

@@ -91,6 +91,7 @@ struct AttnArgs {
   float scale_log2;        // softmax scale * log2(e)
   int4 *items;             // [Hkv][G * NB] workspace: ordered item records per KV group
   int32_t *queue;          // [8] workspace: per-XCD work-queue counters
+  uint16_t *vt;            // [Hkv][NB][B * d] workspace: V^T tiles per key block
 };
 
 // Launchers (each returns the hipError_t of its launch).
