@@ -335,8 +335,10 @@ void sparse_fa_fwd(AttnArgs a) {
   //   fs 2 (next stage top, covered by its wait and barrier): next row complete -> fs 4
   // No load result stays in flight in a register across the stage loop (the compiler
   // would otherwise wait for it, and with it for the K/V DMA, inside the stages).
-  Row nxt;
-  nxt.valid = 0;
+  // the next row is kept as its raw item record (and KV group) until it is used: the derived
+  // Row fields would hold scalar registers over the whole current row
+  int nxt_valid = 0, nxt_g = 0, nxt_x = 0, nxt_y = 0, nxt_z = 0, nxt_w = 0;
+  auto next_row = [&]() { return row_from(nxt_g, nxt_x, nxt_y, nxt_z, nxt_w); };
   int fs = 4, qi = 0, n_fetch = 0, fetch_g = 0;
   const uint32_t rec_off = 4u * (uint32_t)(tid & 3);   // record dword of lanes 0-3
   const uint32_t slot_addr =
@@ -393,9 +395,12 @@ void sparse_fa_fwd(AttnArgs a) {
       }
     } else if (fs == 2) {
       const int4 rec = lds_read_i32x4(rec_addr);
-      nxt = row_from(fetch_g, __builtin_amdgcn_readfirstlane(rec.x),
-                     __builtin_amdgcn_readfirstlane(rec.y), __builtin_amdgcn_readfirstlane(rec.z),
-                     __builtin_amdgcn_readfirstlane(rec.w));
+      nxt_valid = 1;
+      nxt_g = fetch_g;
+      nxt_x = __builtin_amdgcn_readfirstlane(rec.x);
+      nxt_y = __builtin_amdgcn_readfirstlane(rec.y);
+      nxt_z = __builtin_amdgcn_readfirstlane(rec.z);
+      nxt_w = __builtin_amdgcn_readfirstlane(rec.w);
       fs = 4;
     }
   };
@@ -442,9 +447,9 @@ void sparse_fa_fwd(AttnArgs a) {
     fs = 1;
     barrier();
     fetch_finish();
-    if (!nxt.valid) return;
-    cur = nxt;
-    nxt.valid = 0;
+    if (!nxt_valid) return;
+    cur = next_row();
+    nxt_valid = 0;
   }
   int buf = 0;
   int k0_next = stage_first_key<B>(cur, cur.J0, 0);
@@ -494,9 +499,10 @@ void sparse_fa_fwd(AttnArgs a) {
         if (k0_next >= 0) issue(cur, k0_next, buf ^ 1);
       } else {
         fetch_finish();
-        if (nxt.valid) {
-          k0_next = stage_first_key<B>(nxt, nxt.J0, 0);
-          if (k0_next >= 0) issue(nxt, k0_next, buf ^ 1);
+        if (nxt_valid) {
+          const Row nr = next_row();
+          k0_next = stage_first_key<B>(nr, nr.J0, 0);
+          if (k0_next >= 0) issue(nr, k0_next, buf ^ 1);
         }
       }
       buf ^= 1;
@@ -637,9 +643,9 @@ void sparse_fa_fwd(AttnArgs a) {
         }
       }
     }
-    if (!nxt.valid) break;
-    cur = nxt;
-    nxt.valid = 0;
+    if (!nxt_valid) break;
+    cur = next_row();
+    nxt_valid = 0;
   }
 }
 
