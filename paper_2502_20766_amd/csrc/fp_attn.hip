@@ -191,11 +191,26 @@ constexpr int kChunk = 16;   // consecutive ordered items kept together on one X
 
 // Item v of XCD x's work queue -> (KV group g, index j into g's ordered items), false once
 // the queue is exhausted (every later v is then exhausted too).
+//  * Hkv a multiple of 4, at least 8: XCDs x and x + 4 serve groups x % 4, x % 4 + 4, ... in
+//    turn, each group's ordered items dealt to the two in alternate chunks of kChunk.  Only
+//    4 groups' K/V are then read at a time, a working set that fits the last-level cache
+//    (8 Llama-3-8B groups at 128k hold 512 MB of K/V), and similar items stay on one L2;
 //  * Hkv divides 8: the 8/Hkv XCDs that share group g = x mod Hkv take its ordered items in
 //    chunks of kChunk, dealt round-robin, so similar items stay on one XCD's L2;
 //  * otherwise XCD x takes the whole lists of groups x, x + 8, ... in turn (XCDs without a
 //    group only steal).
 __device__ __forceinline__ bool queue_item(int x, int v, int hkv, int n_g, int &g, int &j) {
+  if (hkv % 4 == 0 && hkv >= 8) {
+    const int half = x >> 2;                        // which XCD of the pair
+    const int nch = (n_g + kChunk - 1) / kChunk;    // chunks per group
+    int taken = ((nch - half + 1) / 2) * kChunk;    // items of one group this XCD takes
+    if (((nch - 1) & 1) == half) taken -= nch * kChunk - n_g;   // it holds the short chunk
+    if (taken <= 0) return false;
+    const int q = v / taken, vv = v % taken;
+    g = (x & 3) + 4 * q;
+    j = ((vv / kChunk) * 2 + half) * kChunk + vv % kChunk;
+    return g < hkv && j < n_g;
+  }
   if (8 % hkv == 0) {
     const int r = 8 / hkv;
     g = x % hkv;
