@@ -687,27 +687,32 @@ __device__ __forceinline__ int seq_of_row(const SeqTable &st, int r) {
 // V^T tiles for the attention stages: for KV head h and global key block gb (B keys of
 // one sequence), the B x D slice of V is written as B/16 steps of [d][16 keys], each
 // 16-byte unit (8 keys of one d) at vt_unit(d, key half) of its step -- the order the
-// attention kernel keeps in LDS.  Keys past the sequence end are zero.  Grid: (NB, Hkv).
+// attention kernel keeps in LDS.  Keys past the sequence end are zero.  One tile per call,
+// by the nt threads tid = 0 .. nt-1 of the caller, all of which reach the barrier inside
+// (valid = false: no tile, barrier only).  `tile` is B * D * 2 bytes of LDS.
 template <int D, int B>
-__global__ __launch_bounds__(256) void stage_v_transposed(SeqTable st, const uint16_t *v, int hkv,
-                                                          int nb_total, uint16_t *vt) {
+__device__ __forceinline__ void transpose_v_tile(const SeqTable &st, const uint16_t *v, int hkv,
+                                                 int nb_total, uint16_t *vt, int gb, int h,
+                                                 bool valid, uint4 *tile, int tid, int nt) {
   constexpr int UPR = D / 8;               // 16-byte units per key row of the slice
-  __shared__ uint4 tile[B * UPR];          // [key][d] with the unit index XOR (key % UPR)
-  const int gb = blockIdx.x, h = blockIdx.y;
-  const int s = seq_of_row(st, gb);
-  const int tok = st.cu[s] + (gb - st.nb_off[s]) * B;
-  const int nvalid = min(B, st.cu[s + 1] - tok);
-  for (int u = threadIdx.x; u < B * UPR; u += blockDim.x) {
-    const int key = u / UPR, c = u % UPR;
-    uint4 val = make_uint4(0, 0, 0, 0);
-    if (key < nvalid)
-      val = *reinterpret_cast<const uint4 *>(v + ((int64_t)(tok + key) * hkv + h) * D + 8 * c);
-    tile[key * UPR + (c ^ (key % UPR))] = val;
+  int tok = 0, nvalid = 0;
+  if (valid) {
+    const int s = seq_of_row(st, gb);
+    tok = st.cu[s] + (gb - st.nb_off[s]) * B;
+    nvalid = min(B, st.cu[s + 1] - tok);
+    for (int u = tid; u < B * UPR; u += nt) {  // [key][d], unit index XOR (key % UPR)
+      const int key = u / UPR, c = u % UPR;
+      uint4 val = make_uint4(0, 0, 0, 0);
+      if (key < nvalid)
+        val = *reinterpret_cast<const uint4 *>(v + ((int64_t)(tok + key) * hkv + h) * D + 8 * c);
+      tile[key * UPR + (c ^ (key % UPR))] = val;
+    }
   }
   __syncthreads();
+  if (!valid) return;
   const uint16_t *t16 = reinterpret_cast<const uint16_t *>(tile);
   uint4 *out = reinterpret_cast<uint4 *>(vt + ((int64_t)h * nb_total + gb) * B * D);
-  for (int p = threadIdx.x; p < B * UPR; p += blockDim.x) {
+  for (int p = tid; p < B * UPR; p += nt) {
     const int step = p / (2 * D), w = p % (2 * D);
     const int d = 8 * (w >> 4) + (w & 7);
     const int lh = ((w >> 3) & 1) ^ ((w >> 4) & 1);
@@ -721,6 +726,15 @@ __global__ __launch_bounds__(256) void stage_v_transposed(SeqTable st, const uin
     }
     out[p] = make_uint4(word[0], word[1], word[2], word[3]);
   }
+}
+
+// The V^T tiles alone (used with the plain item order).  Grid: (NB, Hkv), 256 threads.
+template <int D, int B>
+__global__ __launch_bounds__(256) void stage_v_transposed(SeqTable st, const uint16_t *v, int hkv,
+                                                          int nb_total, uint16_t *vt) {
+  __shared__ uint4 tile[B * D / 8];
+  transpose_v_tile<D, B>(st, v, hkv, nb_total, vt, blockIdx.x, blockIdx.y, true, tile,
+                         threadIdx.x, blockDim.x);
 }
 
 // Plain item order, used when a group has too many items for the in-LDS sort: rows by query
@@ -764,12 +778,10 @@ constexpr int kSortItems = 16384;   // items per KV group sorted in LDS (128 KB 
 // alike are adjacent, so that the items running at the same time on an XCD read the same
 // K/V tiles through its L2.  Item id = row * G + kk (heads of a row adjacent).  Also resets
 // the queue counters.
-__global__ __launch_bounds__(1024) void build_item_order_sorted(SeqTable st, const int32_t *kb_idx,
-                                                                const int32_t *kb_cnt, int hq,
-                                                                int hkv, int64_t tri_total,
-                                                                int4 *items, int32_t *queue) {
-  __shared__ unsigned long long key[kSortItems];
-  const int g = blockIdx.x;
+__device__ __forceinline__ void sort_group_items(const SeqTable &st, const int32_t *kb_idx,
+                                                 const int32_t *kb_cnt, int hq, int hkv,
+                                                 int64_t tri_total, int4 *items, int32_t *queue,
+                                                 int g, unsigned long long *key) {
   const int G = hq / hkv;
   const int nb_total = st.nb_off[st.n_seq];
   const int n_g = G * nb_total;
@@ -822,33 +834,58 @@ __global__ __launch_bounds__(1024) void build_item_order_sorted(SeqTable st, con
   }
 }
 
+
+// One launch for both preparations of the attention: workgroups 0 .. Hkv-1 sort their KV
+// group's items (as above), the others write the V^T tiles, four per workgroup (one per 256
+// threads), on the CUs the sort leaves idle.  1024 threads; 128 KB of LDS shared by both.
+template <int D, int B>
+__global__ __launch_bounds__(1024) void prepare_attn(SeqTable st, const int32_t *kb_idx,
+                                                     const int32_t *kb_cnt, int hq, int hkv,
+                                                     int64_t tri_total, int4 *items,
+                                                     int32_t *queue, const uint16_t *v,
+                                                     int nb_total, uint16_t *vt) {
+  static_assert(4 * B * D * 2 <= kSortItems * 8, "V^T tiles exceed the shared LDS");
+  __shared__ __attribute__((aligned(16))) unsigned long long smem[kSortItems];
+  if ((int)blockIdx.x < hkv) {
+    sort_group_items(st, kb_idx, kb_cnt, hq, hkv, tri_total, items, queue, blockIdx.x, smem);
+    return;
+  }
+  const int q = threadIdx.x >> 8;
+  const int t = (blockIdx.x - hkv) * 4 + q;            // tile = gb * Hkv + h
+  const bool valid = t < nb_total * hkv;
+  uint4 *tile = reinterpret_cast<uint4 *>(smem) + q * (B * D / 8);
+  transpose_v_tile<D, B>(st, v, hkv, nb_total, vt, valid ? t / hkv : 0, valid ? t % hkv : 0,
+                         valid, tile, threadIdx.x & 255, 256);
+}
 }  // namespace
 
 hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t stream) {
   const int G = a.hq / a.hkv;
   const int64_t n_g = (int64_t)G * a.nb_total;
-  if (n_g <= kSortItems)
-    hipLaunchKernelGGL(build_item_order_sorted, dim3(a.hkv), dim3(1024), 0, stream, a.st,
-                       a.kb_idx, a.kb_cnt, a.hq, a.hkv, a.tri_total, a.items, a.queue);
-  else
-    hipLaunchKernelGGL(build_item_order_plain, dim3((a.nb_total + 255) / 256), dim3(256), 0,
-                       stream, a.st, a.kb_idx, a.kb_cnt, a.hq, a.hkv, a.tri_total, a.items,
-                       a.queue);
-  const dim3 vt_grid(a.nb_total, a.hkv);
+  // item order and V^T tiles: one fused launch when the groups fit the in-LDS sort
+  auto prepare = [&](auto dc, auto bc) {
+    constexpr int D = decltype(dc)::value, B = decltype(bc)::value;
+    if (n_g <= kSortItems) {
+      const int tiles = a.nb_total * a.hkv;
+      hipLaunchKernelGGL((prepare_attn<D, B>), dim3(a.hkv + (tiles + 3) / 4), dim3(1024), 0,
+                         stream, a.st, a.kb_idx, a.kb_cnt, a.hq, a.hkv, a.tri_total, a.items,
+                         a.queue, a.v, a.nb_total, a.vt);
+    } else {
+      hipLaunchKernelGGL(build_item_order_plain, dim3((a.nb_total + 255) / 256), dim3(256), 0,
+                         stream, a.st, a.kb_idx, a.kb_cnt, a.hq, a.hkv, a.tri_total, a.items,
+                         a.queue);
+      hipLaunchKernelGGL((stage_v_transposed<D, B>), dim3(a.nb_total, a.hkv), dim3(256), 0,
+                         stream, a.st, a.v, a.hkv, a.nb_total, a.vt);
+    }
+  };
+  using I128 = std::integral_constant<int, 128>;
+  using I64 = std::integral_constant<int, 64>;
   if (a.block == 128) {
-    if (a.d == 128)
-      hipLaunchKernelGGL((stage_v_transposed<128, 128>), vt_grid, dim3(256), 0, stream, a.st, a.v,
-                         a.hkv, a.nb_total, a.vt);
-    else
-      hipLaunchKernelGGL((stage_v_transposed<64, 128>), vt_grid, dim3(256), 0, stream, a.st, a.v,
-                         a.hkv, a.nb_total, a.vt);
+    if (a.d == 128) prepare(I128{}, I128{});
+    else prepare(I64{}, I128{});
   } else {
-    if (a.d == 128)
-      hipLaunchKernelGGL((stage_v_transposed<128, 64>), vt_grid, dim3(256), 0, stream, a.st, a.v,
-                         a.hkv, a.nb_total, a.vt);
-    else
-      hipLaunchKernelGGL((stage_v_transposed<64, 64>), vt_grid, dim3(256), 0, stream, a.st, a.v,
-                         a.hkv, a.nb_total, a.vt);
+    if (a.d == 128) prepare(I128{}, I64{});
+    else prepare(I64{}, I64{});
   }
   // Persistent grid: resident workgroups for two waves per SIMD (a multiple of 8, one
   // share per XCD), no more than there are items.
