@@ -256,8 +256,19 @@ __global__ __launch_bounds__(kThreads) void rep_lines(SelectArgs a) {
     if (tid < KT + bp - 1 && jl >= c0 && jl < c1) {
       const int rlo = max(0, bp - 1 - (jl - kt));
       const int rhi = min(bp, bp - 1 - (jl - kt) + KT);
-      float ds = 0.f;
-      for (int rr = rlo; rr < rhi; ++rr) ds += Pt[rr * PT_PITCH + (jl - (bp - 1) + rr - kt)];
+      // element (rr, jl - (bp - 1) + rr - kt) of the tile: stride PT_PITCH + 1 along rr;
+      // eight partial sums keep eight LDS reads in flight (fixed order: deterministic)
+      const float *dp = Pt + (jl - (bp - 1) - kt) + rlo * (PT_PITCH + 1);
+      const int len = rhi - rlo;
+      float d[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      int i = 0;
+      for (; i + 8 <= len; i += 8)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) d[u] += dp[(i + u) * (PT_PITCH + 1)];
+#pragma unroll
+      for (int u = 0; u < 7; ++u)
+        if (i + u < len) d[u] += dp[(i + u) * (PT_PITCH + 1)];
+      const float ds = ((d[0] + d[1]) + (d[2] + d[3])) + ((d[4] + d[5]) + (d[6] + d[7]));
       acc_s[jl - c0] += ds;
     }
     __syncthreads();
