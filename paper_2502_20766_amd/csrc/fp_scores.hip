@@ -44,18 +44,23 @@ __device__ __forceinline__ int k_swz(int chunk, int key) {
   else return chunk ^ ((key >> 1) & 7);
 }
 
-// Keys [kt, kt + KT) of KV head g (rows past n are zero), staged through registers: the
-// next tile is loaded while the current one is in use, then stored to LDS swizzled.
-template <int D>
+// Keys [kt, kt + KT) of KV head g (rows past n are zero), staged through the registers of
+// NT threads: the next tile is loaded while the current one is in use, then stored to LDS
+// swizzled.
+template <int D, int NT = kThreads>
 struct KTile {
   static constexpr int KCH = D / 8;                     // 16-byte chunks per key
-  static constexpr int NIT = KT * KCH / kThreads;       // chunks per thread
+  static constexpr int CH = KT * KCH;                   // chunks per tile
+  static constexpr int NIT = CH >= NT ? CH / NT : 1;    // chunks per thread (threads past
+                                                        // CH stay idle)
+  static_assert(CH < NT || NIT * NT == CH, "tile chunks must divide over the threads");
   uint4 v[NIT];
   __device__ __forceinline__ void load(const uint16_t *kbase, int64_t kv_row, int kt, int n,
                                        int tid) {
 #pragma unroll
     for (int it = 0; it < NIT; ++it) {
-      const int c = it * kThreads + tid;
+      const int c = it * NT + tid;
+      if (CH < NT && c >= CH) continue;
       const int j = kt + c / KCH;
       v[it] = *reinterpret_cast<const uint4 *>(kbase + (int64_t)min(j, n - 1) * kv_row +
                                                (c % KCH) * 8);
@@ -65,7 +70,8 @@ struct KTile {
   __device__ __forceinline__ void store(uint16_t *Ks, int tid) const {
 #pragma unroll
     for (int it = 0; it < NIT; ++it) {
-      const int c = it * kThreads + tid;
+      const int c = it * NT + tid;
+      if (CH < NT && c >= CH) continue;
       const int key = c / KCH;
       *reinterpret_cast<uint4 *>(Ks + key * D + k_swz<D>(c % KCH, key) * 8) = v[it];
     }
@@ -106,18 +112,22 @@ __device__ __forceinline__ void load_qhat(const SelectArgs &a, int tok0, int n, 
 
 // ---------------------------------------------------------------- pass 1: row max / sum
 
-template <int D>
-__global__ __launch_bounds__(kThreads) void rep_stats(SelectArgs a) {
+// HG query heads of one KV group per workgroup (4 waves each), sharing every K tile: the
+// chunk's K is read once for HG heads (HG = 4 fits in 128 registers per lane, so the
+// 16 waves of a workgroup are resident together).
+template <int D, int HG>
+__global__ __launch_bounds__(kThreads * HG) void rep_stats(SelectArgs a) {
+  constexpr int NT = kThreads * HG;
   __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * D];
   const int c = blockIdx.x;
-  const int h = blockIdx.y;
+  const int h = blockIdx.y * HG + (threadIdx.x >> 8);
   const int s = seq_of_chunk(a.st, c);
   const int tok0 = a.st.cu[s];
   const int n = a.st.cu[s + 1] - tok0;
   const int bp = min(a.block, n);
   const int c0 = (c - a.st.ch_off[s]) * kScoreChunk;
   const int c1 = min(c0 + kScoreChunk, n);
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, lr = lane & 31, lh = lane >> 5;
+  const int tid = threadIdx.x, w = (tid >> 6) & 3, lane = tid & 63, lr = lane & 31, lh = lane >> 5;
   const int r = 32 * w + lr;                 // representative row of this lane
   const int irow = n - bp + r;               // its absolute position i_r
   const int G = a.hq / a.hkv;
@@ -128,7 +138,7 @@ __global__ __launch_bounds__(kThreads) void rep_stats(SelectArgs a) {
   bf16x8 qf[D / 16];
   load_qhat<D>(a, tok0, n, h, r, lh, qf);
   float m = -INFINITY, l = 0.f;
-  KTile<D> tile;
+  KTile<D, NT> tile;
   tile.load(kbase, kv_row, c0, n, tid);
   for (int kt = c0; kt < c1; kt += KT) {
     __syncthreads();
@@ -334,10 +344,18 @@ __global__ __launch_bounds__(kThreads) void pool_blocks(SeqTable st, const uint1
 hipError_t launch_rep_scores(const SelectArgs &a, hipStream_t stream) {
   const int ch_total = a.st.ch_off[a.st.n_seq];
   dim3 grid(ch_total, a.hq);
+  // 4 (or 2) query heads of one KV group per workgroup when the group size allows
+  const int G = a.hq / a.hkv;
+  const int hg = G % 4 == 0 ? 4 : (G % 2 == 0 ? 2 : 1);
+  const dim3 grid_g(ch_total, a.hq / hg), block_g(kThreads * hg);
   if (a.d == 128) {
-    hipLaunchKernelGGL(rep_stats<128>, grid, dim3(kThreads), 0, stream, a);
+    if (hg == 4) hipLaunchKernelGGL((rep_stats<128, 4>), grid_g, block_g, 0, stream, a);
+    else if (hg == 2) hipLaunchKernelGGL((rep_stats<128, 2>), grid_g, block_g, 0, stream, a);
+    else hipLaunchKernelGGL((rep_stats<128, 1>), grid_g, block_g, 0, stream, a);
   } else {
-    hipLaunchKernelGGL(rep_stats<64>, grid, dim3(kThreads), 0, stream, a);
+    if (hg == 4) hipLaunchKernelGGL((rep_stats<64, 4>), grid_g, block_g, 0, stream, a);
+    else if (hg == 2) hipLaunchKernelGGL((rep_stats<64, 2>), grid_g, block_g, 0, stream, a);
+    else hipLaunchKernelGGL((rep_stats<64, 1>), grid_g, block_g, 0, stream, a);
   }
   hipLaunchKernelGGL(rep_stats_combine, dim3(a.st.n_seq, a.hq), dim3(128), 0, stream, a);
   if (a.d == 128) {
