@@ -8,9 +8,9 @@
 // One workgroup = one (sequence, query head, query block) row of B queries; B/32 waves of
 // 32 query rows each.  Per selected key block, in stages of B/2 keys:
 //   * K tile [keys][d] is staged in LDS row-major with a 16-byte-chunk XOR swizzle;
-//   * V is transposed once per call (stage_v_transposed) into 16-key steps of V^T,
-//     [step][d][16 keys], already in the swizzled LDS order, so its stage copy is linear
-//     and each V^T fragment is one conflict-free ds_read_b128;
+//   * V is transposed once per call (transpose_v_tile, in the preparation launch) into
+//     16-key steps of V^T, [step][d][16 keys], already in the swizzled LDS order, so its
+//     stage copy is linear and each V^T fragment is one conflict-free ds_read_b128;
 //   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (Q^T fragments live in registers), so each
 //     lane owns one query row and half of the stage's keys: the row max needs one lane
 //     swap.  K rows are read with bits 2 and 3 of the row index swapped, which makes the
@@ -178,7 +178,7 @@ __device__ __forceinline__ void lds_write_i32(uint32_t addr, int v) {
   asm volatile("ds_write_b32 %0, %1" ::"v"(addr), "v"(v) : "memory");
 }
 
-// One unit of work: the 128 queries of (sequence s, query head h, query block I).
+// One unit of work: the B queries of (sequence s, query head h, query block I).
 struct Row {
   int valid;
   int I, h, g, cnt, tok0, n;
@@ -305,8 +305,6 @@ void sparse_fa_fwd(AttnArgs a) {
   const int lane = tid & 63;
   const int lr = lane & 31;
   const int lh = lane >> 5;
-  const int g16 = lane >> 4;
-  const int i16 = lane & 15;
   const int qrow = 32 * w + lr;           // this lane's query row within the block
   const float c = a.scale_log2;
   const int64_t kv_row = (int64_t)a.hkv * D;  // elements between consecutive tokens
@@ -350,8 +348,8 @@ void sparse_fa_fwd(AttnArgs a) {
   //   fs 2 (next stage top, covered by its wait and barrier): next row complete -> fs 4
   // No load result stays in flight in a register across the stage loop (the compiler
   // would otherwise wait for it, and with it for the K/V DMA, inside the stages).
-  // the next row is kept as its raw item record (and KV group) until it is used: the derived
-  // Row fields would hold scalar registers over the whole current row
+  // The next row is kept as its raw item record (and KV group) until it is used: the
+  // derived Row fields would hold scalar registers over the whole current row.
   int nxt_valid = 0, nxt_g = 0, nxt_x = 0, nxt_y = 0, nxt_z = 0, nxt_w = 0;
   auto next_row = [&]() { return row_from(nxt_g, nxt_x, nxt_y, nxt_z, nxt_w); };
   int fs = 4, qi = 0, n_fetch = 0, fetch_g = 0;
