@@ -60,12 +60,13 @@ __device__ __forceinline__ float wave_pair_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// acc + the sum of two 16-key steps' bf16 weights -- exactly the values the P V products
-// use -- two per v_dot2_f32_bf16 against (1, 1).
-__device__ __forceinline__ float sum_weights(const bf16x8 (&pf)[2], float acc) {
+// acc + the sum of N 16-key steps' bf16 weights -- exactly the values the P V products
+// use -- two per v_dot2_f32_bf16 against (1, 1), steps in order.
+template <int N>
+__device__ __forceinline__ float sum_weights(const bf16x8 (&pf)[N], float acc) {
   const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < N; ++i)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const bf16x2 pair = {pf[i][2 * e], pf[i][2 * e + 1]};
@@ -538,22 +539,9 @@ void sparse_fa_fwd(AttnArgs a) {
       for (int k = 0; k < KS; ++k)
         sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[k], qf[k], sacc[b2], 0, 0, 0);
     };
-    auto mask_max = [&](int b2) -> float {
-      if (diag) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = kq + b2 * 32 + 16 * (v >> 3) + 8 * lh + (v & 7);
-          if (key > qrow) sacc[b2][v] = -INFINITY;
-        }
-      }
-      float mt = -INFINITY;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sacc[b2][v]);
-      return wave_pair_max(mt);
-    };
     // Move the reference max when some row of the wave sees a new maximum (rare after the
-    // first blocks), rescaling O and the row sums.  Returns whether it moved.
-    auto update_max = [&](float mt) -> bool {
+    // first blocks), rescaling O and the row sums.
+    auto update_max = [&](float mt) {
       const float m_new = fmaxf(m_ref, mt);
       if (__ballot(m_new > m_ref)) {
         const float alpha = __builtin_amdgcn_exp2f((m_ref - m_new) * c);
@@ -562,14 +550,7 @@ void sparse_fa_fwd(AttnArgs a) {
 #pragma unroll
         for (int i = 0; i < DB; ++i) oacc[i] *= a2;
         m_ref = m_new;
-        return true;
       }
-      return false;
-    };
-    auto weights0 = [&](float (&p0)[16]) {
-      const float mc = (m_ref == -INFINITY) ? 0.f : m_ref * c;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) p0[v] = __builtin_amdgcn_exp2f(fmaf(sacc[0][v], c, -mc));
     };
     // ---- O^T += V^T P^T, 16 keys per step; one ds_read_b128 per V^T fragment
     const uint8_t *vs = lds + ((buf ^ 1) * 2 + 1) * S::BYTES + vaddr_rel;
@@ -583,60 +564,39 @@ void sparse_fa_fwd(AttnArgs a) {
       for (int db = 0; db < DB; ++db)
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db], pf, oacc[db], 0, 0, 0);
     };
-    if constexpr (Geo<B>::SUB == 2) {
-      // sub-block 0 scores and running max
-      qk_block(std::integral_constant<int, 0>{});
-      update_max(mask_max(0));
-      // sub-block 1 scores on MFMA while sub-block 0's weights are computed on VALU
-      qk_block(std::integral_constant<int, 1>{});
-      float p0[16];
-      weights0(p0);
-      // keep these exponentials here, beside sub-block 1's MFMAs (the compiler would
-      // otherwise sink them past the rescale branch below, next to their use)
-      asm volatile("" : "+v"(p0[0]), "+v"(p0[1]), "+v"(p0[2]), "+v"(p0[3]), "+v"(p0[4]),
-                   "+v"(p0[5]), "+v"(p0[6]), "+v"(p0[7]), "+v"(p0[8]), "+v"(p0[9]),
-                   "+v"(p0[10]), "+v"(p0[11]), "+v"(p0[12]), "+v"(p0[13]), "+v"(p0[14]),
-                   "+v"(p0[15]));
-      // sub-block 1 max; if the reference moved, sub-block 0's weights are recomputed
-      if (update_max(mask_max(1))) weights0(p0);
-      bf16x8 pf0[2];
+    // ---- the stage's scores, one running-max update for all its keys, the bf16 weights
+    // (P^T steps of 16 keys) and their sum, then O^T += V^T P^T
+    constexpr int SB = Geo<B>::SUB;
+    qk_block(std::integral_constant<int, 0>{});
+    if constexpr (SB == 2) qk_block(std::integral_constant<int, 1>{});
+    if (diag) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        pf0[0][e] = (__bf16)p0[e];
-        pf0[1][e] = (__bf16)p0[8 + e];
-      }
-      l_run = sum_weights(pf0, l_run);
-
-      pv_step(std::integral_constant<int, 0>{}, pf0[0]);
-      pv_step(std::integral_constant<int, 1>{}, pf0[1]);
-      // sub-block 1 weights (VALU) overlap the PV MFMAs of sub-block 0
-      bf16x8 pf1[2];
-      {
-        const float mc = (m_ref == -INFINITY) ? 0.f : m_ref * c;
+      for (int b2 = 0; b2 < SB; ++b2)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(sacc[1][v], c, -mc));
-          pf1[v >> 3][v & 7] = (__bf16)p;
+          const int key = kq + b2 * 32 + 16 * (v >> 3) + 8 * lh + (v & 7);
+          if (key > qrow) sacc[b2][v] = -INFINITY;
         }
-        l_run = sum_weights(pf1, l_run);
-      }
-      pv_step(std::integral_constant<int, 2>{}, pf1[0]);
-      pv_step(std::integral_constant<int, 3>{}, pf1[1]);
-    } else {
-      // one 32-key sub-block per stage (block 64)
-      qk_block(std::integral_constant<int, 0>{});
-      update_max(mask_max(0));
-      float p0[16];
-      weights0(p0);
-      bf16x8 pf0[2];
+    }
+    float mt = -INFINITY;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        pf0[0][e] = (__bf16)p0[e];
-        pf0[1][e] = (__bf16)p0[8 + e];
-      }
-      l_run = sum_weights(pf0, l_run);
-      pv_step(std::integral_constant<int, 0>{}, pf0[0]);
-      pv_step(std::integral_constant<int, 1>{}, pf0[1]);
+    for (int b2 = 0; b2 < SB; ++b2)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sacc[b2][v]);
+    update_max(wave_pair_max(mt));
+    const float mc = (m_ref == -INFINITY) ? 0.f : m_ref * c;
+    bf16x8 pf[2 * SB];
+#pragma unroll
+    for (int b2 = 0; b2 < SB; ++b2)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        pf[2 * b2 + (v >> 3)][v & 7] = (__bf16)__builtin_amdgcn_exp2f(fmaf(sacc[b2][v], c, -mc));
+    l_run = sum_weights(pf, l_run);
+    pv_step(std::integral_constant<int, 0>{}, pf[0]);
+    pv_step(std::integral_constant<int, 1>{}, pf[1]);
+    if constexpr (SB == 2) {
+      pv_step(std::integral_constant<int, 2>{}, pf[2]);
+      pv_step(std::integral_constant<int, 3>{}, pf[3]);
     }
     }
 
