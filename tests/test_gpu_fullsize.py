@@ -30,12 +30,8 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
-def test_fullsize_selection_and_sampled_outputs(case):
+def _check_layer(name, spec, gamma):
     import paper_2502_20766_amd as fpx
-    name, key, gamma = case
-    spec = synth.SPECS[key]
-    gamma = spec.gamma if gamma is None else gamma
     log(f"[fullsize] {name}: seqlens={spec.seqlens} hq={spec.hq} hkv={spec.hkv} gamma={gamma} "
         f"tau={spec.tau} m={spec.min_budget}")
     with Timer("generate"):
@@ -56,6 +52,24 @@ def test_fullsize_selection_and_sampled_outputs(case):
         mx, mean = compare_outputs(layer, o_host, g["masks"], rows_per_head=4)
     log(f"  output max_abs {mx:.3e} mean_abs {mean:.3e}")
     assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_fullsize_selection_and_sampled_outputs(case):
+    name, key, gamma = case
+    spec = synth.SPECS[key]
+    _check_layer(name, spec, spec.gamma if gamma is None else gamma)
+
+
+def test_maximum_sequence_length():
+    """One sequence at the longest supported length: 8192 blocks of 128 tokens (1,048,576
+    tokens), a vertical-slash and a query-aware head over one KV head.  Every block set is
+    checked against the oracle, outputs on sampled query blocks.  The attention work order of
+    this shape (2 heads x 8192 blocks in the KV group) is exactly the in-LDS sort's capacity."""
+    from synth.layers import LayerSpec
+    spec = LayerSpec("max-2h-n1048576", (1 << 20,), 2, 1, 128, 128, ("vs", "qa"), 16, 0.95,
+                     0.1, 8, 20250228 + 9)
+    _check_layer(spec.name, spec, spec.gamma)
 
 
 @pytest.mark.parametrize("gamma", [0.85, 0.95])
