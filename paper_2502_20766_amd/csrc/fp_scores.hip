@@ -148,16 +148,30 @@ __global__ __launch_bounds__(kThreads * HG) void rep_stats(SelectArgs a) {
     f32x16 sacc[2];
     tile_scores<D>(Ks, qf, lr, lh, sacc);
     float mt = -INFINITY;
+    // masking only in tiles that reach past the chunk, past the first row's position, or
+    // in waves holding rows beyond b' (a wave-uniform test)
+    const bool edge = kt + KT > c1 || kt + KT - 1 > n - bp + 32 * w || 32 * w + 31 >= bp;
+    if (edge) {
 #pragma unroll
-    for (int b2 = 0; b2 < 2; ++b2)
+      for (int b2 = 0; b2 < 2; ++b2)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int j = kt + b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
-        float x = sacc[b2][v] * sl2;
-        if (j >= c1 || j > irow || r >= bp) x = -INFINITY;
-        sacc[b2][v] = x;
-        mt = fmaxf(mt, x);
-      }
+        for (int v = 0; v < 16; ++v) {
+          const int j = kt + b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
+          float x = sacc[b2][v] * sl2;
+          if (j >= c1 || j > irow || r >= bp) x = -INFINITY;
+          sacc[b2][v] = x;
+          mt = fmaxf(mt, x);
+        }
+    } else {
+#pragma unroll
+      for (int b2 = 0; b2 < 2; ++b2)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float x = sacc[b2][v] * sl2;
+          sacc[b2][v] = x;
+          mt = fmaxf(mt, x);
+        }
+    }
     const float mn = fmaxf(m, mt);
     const float mu = (mn == -INFINITY) ? 0.f : mn;
     float acc = 0.f;
@@ -242,16 +256,29 @@ __global__ __launch_bounds__(kThreads) void rep_lines(SelectArgs a) {
     if (kt + KT < c1) tile.load(kbase, kv_row, kt + KT, n, tid);   // overlaps this tile
     f32x16 sacc[2];
     tile_scores<D>(Ks, qf, lr, lh, sacc);
+    // masking only in tiles that reach past the sequence or the first row's position, or
+    // in waves holding rows beyond b' (a wave-uniform test)
+    const bool edge = kt + KT > n || kt + KT - 1 > n - bp + 32 * w || 32 * w + 31 >= bp;
+    if (edge) {
 #pragma unroll
-    for (int b2 = 0; b2 < 2; ++b2)
+      for (int b2 = 0; b2 < 2; ++b2)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int kl = b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
-        const int j = kt + kl;
-        float p = __builtin_amdgcn_exp2f(sacc[b2][v] * sl2 - rm) * rinv;
-        if (j >= n || j > irow || r >= bp) p = 0.f;
-        Pt[r * PT_PITCH + kl] = p;
-      }
+        for (int v = 0; v < 16; ++v) {
+          const int kl = b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
+          const int j = kt + kl;
+          float p = __builtin_amdgcn_exp2f(sacc[b2][v] * sl2 - rm) * rinv;
+          if (j >= n || j > irow || r >= bp) p = 0.f;
+          Pt[r * PT_PITCH + kl] = p;
+        }
+    } else {
+#pragma unroll
+      for (int b2 = 0; b2 < 2; ++b2)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int kl = b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
+          Pt[r * PT_PITCH + kl] = __builtin_amdgcn_exp2f(sacc[b2][v] * sl2 - rm) * rinv;
+        }
+    }
     __syncthreads();
     // vertical lines: column sums over the 128 rows, for owned keys
     if (kt >= c0) {
