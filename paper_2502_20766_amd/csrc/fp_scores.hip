@@ -235,11 +235,11 @@ __global__ __launch_bounds__(kThreads) void rep_lines(SelectArgs a) {
   const uint16_t *kbase = a.k + (int64_t)tok0 * kv_row + (int64_t)(h / G) * D;
   const float sl2 = a.scale * 1.4426950408889634f;
 
-  float rm = 0.f, rinv = 0.f;
+  // Â[r, j] = exp2(s_rj * sl2 - m_r) / (l_r * b') = exp2(s_rj * sl2 - m_r - log2(l_r * b'))
+  float rm = 0.f;
   if (r < bp) {
     const float2 st = a.row_stats[((int64_t)s * a.hq + h) * a.block + r];
-    rm = st.x;
-    rinv = 1.f / (st.y * (float)bp);
+    rm = st.x + __builtin_amdgcn_logf(st.y * (float)bp);
   }
   bf16x8 qf[D / 16];
   load_qhat<D>(a, tok0, n, h, r, lh, qf);
@@ -266,7 +266,7 @@ __global__ __launch_bounds__(kThreads) void rep_lines(SelectArgs a) {
         for (int v = 0; v < 16; ++v) {
           const int kl = b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
           const int j = kt + kl;
-          float p = __builtin_amdgcn_exp2f(sacc[b2][v] * sl2 - rm) * rinv;
+          float p = __builtin_amdgcn_exp2f(sacc[b2][v] * sl2 - rm);
           if (j >= n || j > irow || r >= bp) p = 0.f;
           Pt[r * PT_PITCH + kl] = p;
         }
@@ -276,7 +276,7 @@ __global__ __launch_bounds__(kThreads) void rep_lines(SelectArgs a) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int kl = b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
-          Pt[r * PT_PITCH + kl] = __builtin_amdgcn_exp2f(sacc[b2][v] * sl2 - rm) * rinv;
+          Pt[r * PT_PITCH + kl] = __builtin_amdgcn_exp2f(sacc[b2][v] * sl2 - rm);
         }
     }
     __syncthreads();
