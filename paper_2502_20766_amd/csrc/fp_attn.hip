@@ -103,13 +103,17 @@ __device__ __forceinline__ int vt_unit(int d, int lh) {
 }
 
 // Per-lane byte offsets of the DMA slots of one stage, relative to the stage's first key
-// row (K) or first byte (V^T): slot i of wave w covers LDS bytes [(WAVES i + w) * 1024,
-// +1024); for K lane l fills 16 bytes of tile row r with the logical chunk whose swizzled
-// position is the lane's slot, for V^T (stored in LDS order) the copy is linear.
+// row (K) or first byte (V^T): slot i of wave w covers LDS bytes [(DMA_PER_WAVE w + i)
+// * 1024, +1024); for K lane l fills 16 bytes of tile row r with the logical chunk whose
+// swizzled position is the lane's slot, for V^T (stored in LDS order) the copy is linear.
+// A wave's slots are contiguous so that one M0 value serves all of them: the instruction's
+// immediate offset (i * 1024) moves both the LDS destination and the source address, and
+// the per-lane offsets below have it taken off.  The descriptor's range check applies to
+// the sum, so K rows past the valid range still read as zero.
 template <int D, int B>
 struct DmaOffsets {
   uint32_t k[Stage<D, B>::DMA_PER_WAVE];
-  uint32_t v[Stage<D, B>::DMA_PER_WAVE];
+  uint32_t v;
 };
 
 template <int D, int B>
@@ -118,12 +122,12 @@ __device__ __forceinline__ DmaOffsets<D, B> dma_offsets(uint32_t row_bytes, int 
   DmaOffsets<D, B> o;
 #pragma unroll
   for (int i = 0; i < S::DMA_PER_WAVE; ++i) {
-    const int q = i * Geo<B>::WAVES + w;
+    const int q = w * S::DMA_PER_WAVE + i;
     const int r = q * S::RPI + lane / S::CPR;
     const int phys = lane % S::CPR;
-    o.k[i] = r * row_bytes + swz_k<D>(phys, r) * 16;
-    o.v[i] = q * 1024 + lane * 16;
+    o.k[i] = r * row_bytes + swz_k<D>(phys, r) * 16 - i * 1024;
   }
+  o.v = w * S::DMA_PER_WAVE * 1024 + lane * 16;
   return o;
 }
 
@@ -140,6 +144,28 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void *base,
                                            0x00020000);
 }
 
+// Wave-wide 16-byte DMAs into LDS slots I .. N-1, slot i at i * 1024 past `dst` (the
+// immediate offset moves the source address by the same amount), with a per-lane offset
+// per slot (K) or one shared by all slots (V^T).
+template <int I, int N>
+__device__ __forceinline__ void dma_slots(__amdgpu_buffer_rsrc_t r,
+                                          __attribute__((address_space(3))) void *dst,
+                                          const uint32_t *voff) {
+  if constexpr (I < N) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff[I], 0, I * 1024, 0);
+    dma_slots<I + 1, N>(r, dst, voff);
+  }
+}
+template <int I, int N>
+__device__ __forceinline__ void dma_slots(__amdgpu_buffer_rsrc_t r,
+                                          __attribute__((address_space(3))) void *dst,
+                                          uint32_t voff) {
+  if constexpr (I < N) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, 0, I * 1024, 0);
+    dma_slots<I + 1, N>(r, dst, voff);
+  }
+}
+
 // Issue the DMA of one stage: keys k0 .. k0+KEYS-1 of the sequence, K through a buffer
 // descriptor whose range ends at the last valid key row (rows past the sequence end read
 // as zeros and are masked by the caller), V^T as the stage's contiguous tile (zero past
@@ -152,15 +178,12 @@ __device__ __forceinline__ void stage_dma(uint8_t *ks, uint8_t *vs, const uint16
   const int nrec = (kvalid - 1) * (int)kv_row * 2 + 2 * D;
   const __amdgpu_buffer_rsrc_t rk = uniform_rsrc(kbase + (int64_t)k0 * kv_row, nrec);
   const __amdgpu_buffer_rsrc_t rv = uniform_rsrc(vt_tile, S::BYTES);
+  static_assert((S::DMA_PER_WAVE - 1) * 1024 < 4096, "immediate offsets are 12 bits");
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-#pragma unroll
-  for (int i = 0; i < S::DMA_PER_WAVE; ++i) {
-    const int q = i * Geo<B>::WAVES + w;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        rk, (__attribute__((address_space(3))) void *)(ks + q * 1024), 16, off.k[i], 0, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        rv, (__attribute__((address_space(3))) void *)(vs + q * 1024), 16, off.v[i], 0, 0, 0);
-  }
+  auto *kd = (__attribute__((address_space(3))) void *)(ks + w * S::DMA_PER_WAVE * 1024);
+  auto *vd = (__attribute__((address_space(3))) void *)(vs + w * S::DMA_PER_WAVE * 1024);
+  dma_slots<0, S::DMA_PER_WAVE>(rk, kd, off.k);
+  dma_slots<0, S::DMA_PER_WAVE>(rv, vd, off.v);
 }
 
 // Small LDS accesses whose ordering against the in-flight LDS DMA is handled by the
@@ -382,6 +405,7 @@ void sparse_fa_fwd(AttnArgs a) {
   auto fetch_step = [&]() {
     if (fs == 1) {
       while (true) {
+        qi = __builtin_amdgcn_readfirstlane(qi);
         const int x = (x0 + qi) & 7;
         const int v =
             P8 + __builtin_amdgcn_readfirstlane(lds_read_i32(slot_addr + 4 * (n_fetch & 1)));
@@ -417,6 +441,11 @@ void sparse_fa_fwd(AttnArgs a) {
       nxt_w = __builtin_amdgcn_readfirstlane(rec.w);
       fs = 4;
     }
+    // (the compiler's uniformity analysis does not always see through the loop above)
+    fs = __builtin_amdgcn_readfirstlane(fs);
+    qi = __builtin_amdgcn_readfirstlane(qi);
+    n_fetch = __builtin_amdgcn_readfirstlane(n_fetch);
+    nxt_valid = __builtin_amdgcn_readfirstlane(nxt_valid);
   };
   // complete the fetch now (rows with fewer stages than fetch steps)
   auto fetch_finish = [&]() {

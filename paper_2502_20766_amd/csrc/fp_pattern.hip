@@ -56,8 +56,11 @@ __device__ __forceinline__ float block_max(float v, float *scratch) {
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void pattern_search(SelectArgs a) {
+  constexpr int CH = D / 8;                 // 16-byte chunks of a query row
+  constexpr int PH = kThreads / CH;         // row phases of the Q_hat pooling
   extern __shared__ float dyn[];            // [max_nb] logits
-  __shared__ float qbar[D];
+  __shared__ __attribute__((aligned(16))) float qbar[D];
+  __shared__ float qpart[PH][D];
   __shared__ float fscr[kThreads];
   __shared__ double dscr[kThreads];
   const int s = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
@@ -68,21 +71,50 @@ __global__ __launch_bounds__(kThreads) void pattern_search(SelectArgs a) {
   const int G = a.hq / a.hkv;
   const int g = h / G;
 
-  // avgpool(Q_hat): mean of the last b' query rows
+  // avgpool(Q_hat): thread (phase ph, chunk ch) sums rows ph, ph + PH, ... of its 8
+  // dimensions; the phases are then added in order
+  {
+    const int ch = tid % CH, ph = tid / CH;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    const uint16_t *qp = a.q + ((int64_t)(tok0 + n - bp) * a.hq + h) * D + ch * 8;
+#pragma unroll 4
+    for (int r = ph; r < bp; r += PH) {
+      const uint4 v = *reinterpret_cast<const uint4 *>(qp + (int64_t)r * a.hq * D);
+      const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[2 * i] += __uint_as_float(wv[i] << 16);
+        acc[2 * i + 1] += __uint_as_float(wv[i] & 0xFFFF0000u);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) qpart[ph][ch * 8 + i] = acc[i];
+  }
+  __syncthreads();
   if (tid < D) {
     float acc = 0.f;
-    const uint16_t *qp = a.q + ((int64_t)(tok0 + n - bp) * a.hq + h) * D + tid;
-    for (int r = 0; r < bp; ++r) acc += __uint_as_float((uint32_t)qp[(int64_t)r * a.hq * D] << 16);
+    for (int ph = 0; ph < PH; ++ph) acc += qpart[ph][tid];
     qbar[tid] = acc / (float)bp;
   }
   __syncthreads();
-  // logits over key blocks
+  // logits over key blocks (one block per thread, its pooled key read as 16-byte vectors)
   float mx = -INFINITY;
   for (int J = tid; J < nb; J += kThreads) {
-    const float *kb = a.kbar + ((int64_t)(a.st.nb_off[s] + J) * a.hkv + g) * D;
+    const float4 *kb =
+        reinterpret_cast<const float4 *>(a.kbar + ((int64_t)(a.st.nb_off[s] + J) * a.hkv + g) * D);
+    float4 kv[D / 4];
+#pragma unroll
+    for (int i = 0; i < D / 4; ++i) kv[i] = kb[i];
+    const float4 *q4 = reinterpret_cast<const float4 *>(qbar);
     float dot = 0.f;
-#pragma unroll 8
-    for (int d = 0; d < D; ++d) dot = fmaf(qbar[d], kb[d], dot);
+#pragma unroll
+    for (int i = 0; i < D / 4; ++i) {
+      const float4 qv = q4[i];
+      dot = fmaf(qv.x, kv[i].x, dot);
+      dot = fmaf(qv.y, kv[i].y, dot);
+      dot = fmaf(qv.z, kv[i].z, dot);
+      dot = fmaf(qv.w, kv[i].w, dot);
+    }
     const float x = dot * a.scale;
     dyn[J] = x;
     mx = fmaxf(mx, x);
@@ -97,8 +129,21 @@ __global__ __launch_bounds__(kThreads) void pattern_search(SelectArgs a) {
   for (int J = tid; J < nb; J += kThreads) {
     const double pb = (double)expf(dyn[J] - mx) / se;              // a_bar[J]
     double ph = 0.0;                                                // a_hat[J]
-    const int j1 = min((J + 1) * a.block, n);
-    for (int j = J * a.block; j < j1; ++j) ph += (double)av[j];
+    const int j0 = J * a.block, j1 = min(j0 + a.block, n);
+    const float *ap = av + j0;
+    int j = 0;
+    if ((reinterpret_cast<uintptr_t>(ap) & 15) == 0) {
+      // 16-byte loads, eight in flight; the sum stays in token order
+      for (; j + 32 <= j1 - j0; j += 32) {
+        float4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = reinterpret_cast<const float4 *>(ap + j)[u];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          ph = (((ph + (double)v[u].x) + (double)v[u].y) + (double)v[u].z) + (double)v[u].w;
+      }
+    }
+    for (; j < j1 - j0; ++j) ph += (double)ap[j];
     const double m = 0.5 * (pb + ph);
     if (pb > 0.0) jsd += 0.5 * pb * log(pb / m);
     if (ph > 0.0) jsd += 0.5 * ph * log(ph / m);
@@ -119,11 +164,13 @@ constexpr int QT = 64;   // rows and columns of A_bar per workgroup tile
 
 // Tile (TI, TJ), TJ <= TI, of the logits scale * Q_bar_I . K_bar_J written into the
 // flattened causal layout.  Grid x enumerates the causal tile pairs of all sequences.
+// Each wave computes one 32x32 quarter with the fp32 MFMA (products and sums in fp32,
+// as the vector code would): lane (l % 32, l / 32) supplies Q_bar row l % 32 and
+// K_bar row l % 32 over dimensions [l / 32 * D / 2, +D / 2), so the reduction runs over
+// the same dimensions for both operands, read straight from global memory (L2-resident).
 template <int D>
 __global__ __launch_bounds__(kThreads) void qa_logits(SelectArgs a) {
-  constexpr int DC = 64;                 // d staged per step
-  __shared__ float Qs[QT][DC + 1];
-  __shared__ float Ks[QT][DC + 1];
+  typedef float f32x16 __attribute__((ext_vector_type(16)));
   const int h = blockIdx.y;
   // locate sequence and tile pair
   int t = blockIdx.x, s = 0, nt = 0;
@@ -143,40 +190,38 @@ __global__ __launch_bounds__(kThreads) void qa_logits(SelectArgs a) {
   const int nb = a.st.nb_off[s + 1] - a.st.nb_off[s];
   const int G = a.hq / a.hkv;
   const int g = h / G;
-  const int tid = threadIdx.x;
-  const int ti = tid / 16, tj = tid % 16;
-  float acc[4][4] = {};
-  for (int d0 = 0; d0 < D; d0 += DC) {
-    __syncthreads();
-    for (int i = tid; i < QT * DC; i += kThreads) {
-      const int row = i / DC, d = d0 + i % DC;
-      const int I = TI * QT + row, J = TJ * QT + row;
-      Qs[row][i % DC] = I < nb ? a.qbar[((int64_t)(a.st.nb_off[s] + I) * a.hq + h) * D + d] : 0.f;
-      Ks[row][i % DC] = J < nb ? a.kbar[((int64_t)(a.st.nb_off[s] + J) * a.hkv + g) * D + d] : 0.f;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, lr = lane & 31, lh = lane >> 5;
+  const int I0 = TI * QT + 32 * (w >> 1), J0 = TJ * QT + 32 * (w & 1);
+  if (J0 > I0 + 31 || I0 >= nb) return;      // quarter above the diagonal or past the end
+  const int Ir = min(I0 + lr, nb - 1), Jr = min(J0 + lr, nb - 1);
+  const float4 *qp = reinterpret_cast<const float4 *>(
+      a.qbar + ((int64_t)(a.st.nb_off[s] + Ir) * a.hq + h) * D + lh * (D / 2));
+  const float4 *kp = reinterpret_cast<const float4 *>(
+      a.kbar + ((int64_t)(a.st.nb_off[s] + Jr) * a.hkv + g) * D + lh * (D / 2));
+  f32x16 acc = {};
+#pragma unroll
+  for (int c = 0; c < D / 8; c += 4) {
+    float4 qv[4], kv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      qv[u] = qp[c + u];
+      kv[u] = kp[c + u];
     }
-    __syncthreads();
-    for (int d = 0; d < DC; ++d) {
-      float qv[4], kv[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        qv[i] = Qs[ti + 16 * i][d];
-        kv[i] = Ks[tj + 16 * i][d];
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(qv[i], kv[j], acc[i][j]);
+    for (int u = 0; u < 4; ++u) {
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qv[u].x, kv[u].x, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qv[u].y, kv[u].y, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qv[u].z, kv[u].z, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qv[u].w, kv[u].w, acc, 0, 0, 0);
     }
   }
+  // lane holds column J0 + lr of rows I0 + 8 (v / 4) + 4 lh + v % 4
   float *flat = a.flat + (int64_t)h * a.tri_total + a.st.tri_off[s];
+  const int J = J0 + lr;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int I = TI * QT + ti + 16 * i;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int J = TJ * QT + tj + 16 * j;
-      if (I < nb && J <= I) flat[(int64_t)I * (I + 1) / 2 + J] = acc[i][j] * a.scale;
-    }
+  for (int v = 0; v < 16; ++v) {
+    const int I = I0 + 8 * (v >> 2) + 4 * lh + (v & 3);
+    if (I < nb && J <= I) flat[(int64_t)I * (I + 1) / 2 + J] = acc[v] * a.scale;
   }
 }
 
