@@ -14,6 +14,8 @@
 //
 // Block pooling (avgpool with window block_size, aligned at token 0 of each sequence) is
 // a separate streaming kernel used for K (all KV heads) and Q (query-aware heads only).
+#include <type_traits>
+
 #include "fp_internal.h"
 
 namespace fp {
@@ -78,8 +80,10 @@ struct KTile {
   }
 };
 
-// S^T for 64 keys x the wave's 32 query rows: two 32x32 MFMA blocks.
-template <int D>
+// Scores of 64 keys x the wave's 32 query rows: two 32x32 MFMA blocks.  KEY_ROWS: S^T (lane
+// holds query row lane % 32 and 16 keys); otherwise S (lane holds key lane % 32 of the
+// sub-block and 16 query rows).  The fragments are the same, only the operand order differs.
+template <int D, bool KEY_ROWS = true>
 __device__ __forceinline__ void tile_scores(const uint16_t *Ks, const bf16x8 *qf, int lr, int lh,
                                             f32x16 *sacc) {
 #pragma unroll
@@ -90,7 +94,10 @@ __device__ __forceinline__ void tile_scores(const uint16_t *Ks, const bf16x8 *qf
     for (int k = 0; k < D / 16; ++k) {
       const bf16x8 kf =
           *reinterpret_cast<const bf16x8 *>(Ks + key * D + k_swz<D>(2 * k + lh, key) * 8);
-      sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], sacc[b2], 0, 0, 0);
+      if constexpr (KEY_ROWS)
+        sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], sacc[b2], 0, 0, 0);
+      else
+        sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[k], kf, sacc[b2], 0, 0, 0);
     }
   }
 }
@@ -196,19 +203,29 @@ __global__ __launch_bounds__(kThreads * HG) void rep_stats(SelectArgs a) {
     a.chunk_stats[((int64_t)c * a.hq + h) * a.block + r] = make_float2(mm, lt);
 }
 
-// Merge the chunk statistics of each representative row, in chunk order.
-__global__ void rep_stats_combine(SelectArgs a) {
-  const int s = blockIdx.x, h = blockIdx.y, r = threadIdx.x;
+// (m1, l1) + (m2, l2) in log2 units: the max and the sum of exp2 rescaled to it.
+__device__ __forceinline__ float2 merge_stats(float2 p, float2 q) {
+  const float mn = fmaxf(p.x, q.x);
+  const float mu = (mn == -INFINITY) ? 0.f : mn;
+  return make_float2(mn, p.y * __builtin_amdgcn_exp2f(p.x - mu) + q.y * __builtin_amdgcn_exp2f(q.x - mu));
+}
+
+// Merge the chunk statistics of each representative row: one wave per row, lane i merges
+// chunks i, i + 64, ... in order, then a butterfly over the lanes in which each pair is
+// merged lower lane first (every lane computes the same value; the result is fixed).
+__global__ __launch_bounds__(256) void rep_stats_combine(SelectArgs a) {
+  const int s = blockIdx.x, h = blockIdx.y;
+  const int r = blockIdx.z * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (r >= a.block) return;
-  float m = -INFINITY, l = 0.f;
-  for (int c = a.st.ch_off[s]; c < a.st.ch_off[s + 1]; ++c) {
-    const float2 p = a.chunk_stats[((int64_t)c * a.hq + h) * a.block + r];
-    const float mn = fmaxf(m, p.x);
-    const float mu = (mn == -INFINITY) ? 0.f : mn;
-    l = l * __builtin_amdgcn_exp2f(m - mu) + p.y * __builtin_amdgcn_exp2f(p.x - mu);
-    m = mn;
+  float2 acc = make_float2(-INFINITY, 0.f);
+  for (int c = a.st.ch_off[s] + lane; c < a.st.ch_off[s + 1]; c += 64)
+    acc = merge_stats(acc, a.chunk_stats[((int64_t)c * a.hq + h) * a.block + r]);
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float2 o = make_float2(__shfl_xor(acc.x, off), __shfl_xor(acc.y, off));
+    acc = (lane & off) ? merge_stats(o, acc) : merge_stats(acc, o);
   }
-  a.row_stats[((int64_t)s * a.hq + h) * a.block + r] = make_float2(m, l);
+  if (lane == 0) a.row_stats[((int64_t)s * a.hq + h) * a.block + r] = acc;
 }
 
 // ---------------------------------------------------------------- pass 2: line sums
@@ -229,17 +246,23 @@ __global__ __launch_bounds__(kThreads) void rep_lines(SelectArgs a) {
   const int c1 = min(c0 + kScoreChunk, n);
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, lr = lane & 31, lh = lane >> 5;
   const int r = 32 * w + lr;
-  const int irow = n - bp + r;
   const int G = a.hq / a.hkv;
   const int64_t kv_row = (int64_t)a.hkv * D;
   const uint16_t *kbase = a.k + (int64_t)tok0 * kv_row + (int64_t)(h / G) * D;
   const float sl2 = a.scale * 1.4426950408889634f;
 
-  // Â[r, j] = exp2(s_rj * sl2 - m_r) / (l_r * b') = exp2(s_rj * sl2 - m_r - log2(l_r * b'))
-  float rm = 0.f;
-  if (r < bp) {
-    const float2 st = a.row_stats[((int64_t)s * a.hq + h) * a.block + r];
-    rm = st.x + __builtin_amdgcn_logf(st.y * (float)bp);
+  // Â[r, j] = exp2(s_rj * sl2 - m_r) / (l_r * b') = exp2(s_rj * sl2 - m_r - log2(l_r * b')).
+  // The scores are computed as S = Q_hat K^T: lane (lr, lh) holds key lr of each 32-key
+  // sub-block for the 16 rows rv(v) = 32 w + 8 (v / 4) + 4 lh + v % 4.
+  float rm[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int rv = 32 * w + 8 * (v >> 2) + 4 * lh + (v & 3);
+    rm[v] = 0.f;
+    if (rv < bp) {
+      const float2 st = a.row_stats[((int64_t)s * a.hq + h) * a.block + rv];
+      rm[v] = st.x + __builtin_amdgcn_logf(st.y * (float)bp);
+    }
   }
   bf16x8 qf[D / 16];
   load_qhat<D>(a, tok0, n, h, r, lh, qf);
@@ -255,38 +278,41 @@ __global__ __launch_bounds__(kThreads) void rep_lines(SelectArgs a) {
     __syncthreads();
     if (kt + KT < c1) tile.load(kbase, kv_row, kt + KT, n, tid);   // overlaps this tile
     f32x16 sacc[2];
-    tile_scores<D>(Ks, qf, lr, lh, sacc);
+    tile_scores<D, false>(Ks, qf, lr, lh, sacc);
     // masking only in tiles that reach past the sequence or the first row's position, or
     // in waves holding rows beyond b' (a wave-uniform test)
     const bool edge = kt + KT > n || kt + KT - 1 > n - bp + 32 * w || 32 * w + 31 >= bp;
-    if (edge) {
+    float cs[2];
+    auto weights = [&](auto masked) {
 #pragma unroll
-      for (int b2 = 0; b2 < 2; ++b2)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int kl = b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
-          const int j = kt + kl;
-          float p = __builtin_amdgcn_exp2f(sacc[b2][v] * sl2 - rm);
-          if (j >= n || j > irow || r >= bp) p = 0.f;
-          Pt[r * PT_PITCH + kl] = p;
-        }
-    } else {
-#pragma unroll
-      for (int b2 = 0; b2 < 2; ++b2)
+      for (int b2 = 0; b2 < 2; ++b2) {
+        const int kl = b2 * 32 + lr;
+        const int j = kt + kl;
+        cs[b2] = 0.f;
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int kl = b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
-          Pt[r * PT_PITCH + kl] = __builtin_amdgcn_exp2f(sacc[b2][v] * sl2 - rm);
+          const int rv = 32 * w + 8 * (v >> 2) + 4 * lh + (v & 3);
+          float p = __builtin_amdgcn_exp2f(sacc[b2][v] * sl2 - rm[v]);
+          if constexpr (decltype(masked)::value)
+            p = ((j < n) & (j <= n - bp + rv) & (rv < bp)) ? p : 0.f;
+          Pt[rv * PT_PITCH + kl] = p;
+          cs[b2] += p;
         }
+      }
+    };
+    if (edge) weights(std::true_type{});
+    else weights(std::false_type{});
+    // vertical lines: this lane's 16 rows, then the other lane half's (lower half first),
+    // then the four waves in order after the barrier
+    if (kt >= c0) {
+#pragma unroll
+      for (int b2 = 0; b2 < 2; ++b2) {
+        const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(cs[b2]),
+                                                         __float_as_uint(cs[b2]), false, false);
+        if (lh == 0) red[w][b2 * 32 + lr] = __uint_as_float(pr[0]) + __uint_as_float(pr[1]);
+      }
     }
     __syncthreads();
-    // vertical lines: column sums over the 128 rows, for owned keys
-    if (kt >= c0) {
-      const int col = tid & (KT - 1), quarter = tid >> 6;
-      float cs = 0.f;
-      for (int rr = 32 * quarter; rr < 32 * quarter + 32; ++rr) cs += Pt[rr * PT_PITCH + col];
-      red[quarter][col] = cs;
-    }
     // slash lines: diagonal o with last-row key jl = n - 1 - o meets this tile for
     // jl in [kt, kt + KT + bp - 1); rows r with key jl - (bp - 1) + r inside the tile
     const int jl = kt + tid;
@@ -384,7 +410,8 @@ hipError_t launch_rep_scores(const SelectArgs &a, hipStream_t stream) {
     else if (hg == 2) hipLaunchKernelGGL((rep_stats<64, 2>), grid_g, block_g, 0, stream, a);
     else hipLaunchKernelGGL((rep_stats<64, 1>), grid_g, block_g, 0, stream, a);
   }
-  hipLaunchKernelGGL(rep_stats_combine, dim3(a.st.n_seq, a.hq), dim3(128), 0, stream, a);
+  hipLaunchKernelGGL(rep_stats_combine, dim3(a.st.n_seq, a.hq, (a.block + 3) / 4), dim3(256), 0,
+                     stream, a);
   if (a.d == 128) {
     hipLaunchKernelGGL(rep_lines<128>, grid, dim3(kThreads), 0, stream, a);
     hipLaunchKernelGGL(pool_blocks<128>, dim3(a.nb_total, a.hkv), dim3(kThreads), 0, stream, a.st,
