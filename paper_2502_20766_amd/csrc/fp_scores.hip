@@ -46,13 +46,13 @@ __device__ __forceinline__ int k_swz(int chunk, int key) {
   else return chunk ^ ((key >> 1) & 7);
 }
 
-// Keys [kt, kt + KT) of KV head g (rows past n are zero), staged through the registers of
+// Keys [kt, kt + TK) of KV head g (rows past n are zero), staged through the registers of
 // NT threads: the next tile is loaded while the current one is in use, then stored to LDS
 // swizzled.
-template <int D, int NT = kThreads>
+template <int D, int NT = kThreads, int TK = KT>
 struct KTile {
   static constexpr int KCH = D / 8;                     // 16-byte chunks per key
-  static constexpr int CH = KT * KCH;                   // chunks per tile
+  static constexpr int CH = TK * KCH;                   // chunks per tile
   static constexpr int NIT = CH >= NT ? CH / NT : 1;    // chunks per thread (threads past
                                                         // CH stay idle)
   static_assert(CH < NT || NIT * NT == CH, "tile chunks must divide over the threads");
@@ -230,12 +230,22 @@ __global__ __launch_bounds__(256) void rep_stats_combine(SelectArgs a) {
 
 // ---------------------------------------------------------------- pass 2: line sums
 
+// 32-key tiles: each wave computes S = Q_hat K^T for its 32 rows and the tile's 32 keys
+// with one MFMA block, so a lane holds one key and 16 rows and the column sums (vertical
+// lines) are in-lane adds plus one half-wave swap.  The weights go to an LDS tile whose
+// diagonals (slash lines) are summed by the workgroup.  The small tile keeps the LDS and
+// register footprint low enough for four workgroups per CU, which hides the latency of
+// the barrier-separated phases.
+constexpr int LKT = 32;                        // keys per line-pass tile
+constexpr int LPITCH = LKT + 1;                // odd pitch: diagonal reads are conflict free
+
 template <int D>
-__global__ __launch_bounds__(kThreads) void rep_lines(SelectArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * D];
-  __shared__ float Pt[128 * PT_PITCH];         // A_hat tile / b', [row][key]
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void rep_lines(
+    SelectArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[LKT * D];
+  __shared__ float Pt[128 * LPITCH];           // Â tile, [row][key]
   __shared__ float acc_s[kScoreChunk];         // owned slash offsets
-  __shared__ float red[4][KT];
+  __shared__ float red[4][LKT];                // per wave: column sums of the tile
   const int c = blockIdx.x;
   const int h = blockIdx.y;
   const int s = seq_of_chunk(a.st, c);
@@ -252,8 +262,8 @@ __global__ __launch_bounds__(kThreads) void rep_lines(SelectArgs a) {
   const float sl2 = a.scale * 1.4426950408889634f;
 
   // Â[r, j] = exp2(s_rj * sl2 - m_r) / (l_r * b') = exp2(s_rj * sl2 - m_r - log2(l_r * b')).
-  // The scores are computed as S = Q_hat K^T: lane (lr, lh) holds key lr of each 32-key
-  // sub-block for the 16 rows rv(v) = 32 w + 8 (v / 4) + 4 lh + v % 4.
+  // Lane (lr, lh) holds key lr of the tile for the 16 rows rv(v) = 32 w + 8 (v / 4) + 4 lh
+  // + v % 4.
   float rm[16];
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
@@ -270,34 +280,34 @@ __global__ __launch_bounds__(kThreads) void rep_lines(SelectArgs a) {
 
   // keys [c0 - 128, c0) are recomputed for the diagonals owned by this chunk
   const int kstart = max(c0 - 128, 0);
-  KTile<D> tile;
+  KTile<D, kThreads, LKT> tile;
   tile.load(kbase, kv_row, kstart, n, tid);
-  for (int kt = kstart; kt < c1; kt += KT) {
+  for (int kt = kstart; kt < c1; kt += LKT) {
     __syncthreads();
     tile.store(Ks, tid);
     __syncthreads();
-    if (kt + KT < c1) tile.load(kbase, kv_row, kt + KT, n, tid);   // overlaps this tile
-    f32x16 sacc[2];
-    tile_scores<D, false>(Ks, qf, lr, lh, sacc);
+    if (kt + LKT < c1) tile.load(kbase, kv_row, kt + LKT, n, tid);   // overlaps this tile
+    f32x16 sacc = {};
+#pragma unroll
+    for (int k = 0; k < D / 16; ++k) {
+      const bf16x8 kf =
+          *reinterpret_cast<const bf16x8 *>(Ks + lr * D + k_swz<D>(2 * k + lh, lr) * 8);
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[k], kf, sacc, 0, 0, 0);
+    }
     // masking only in tiles that reach past the sequence or the first row's position, or
     // in waves holding rows beyond b' (a wave-uniform test)
-    const bool edge = kt + KT > n || kt + KT - 1 > n - bp + 32 * w || 32 * w + 31 >= bp;
-    float cs[2];
+    const bool edge = kt + LKT > n || kt + LKT - 1 > n - bp + 32 * w || 32 * w + 31 >= bp;
+    const int j = kt + lr;
+    float cs = 0.f;
     auto weights = [&](auto masked) {
 #pragma unroll
-      for (int b2 = 0; b2 < 2; ++b2) {
-        const int kl = b2 * 32 + lr;
-        const int j = kt + kl;
-        cs[b2] = 0.f;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int rv = 32 * w + 8 * (v >> 2) + 4 * lh + (v & 3);
-          float p = __builtin_amdgcn_exp2f(sacc[b2][v] * sl2 - rm[v]);
-          if constexpr (decltype(masked)::value)
-            p = ((j < n) & (j <= n - bp + rv) & (rv < bp)) ? p : 0.f;
-          Pt[rv * PT_PITCH + kl] = p;
-          cs[b2] += p;
-        }
+      for (int v = 0; v < 16; ++v) {
+        const int rv = 32 * w + 8 * (v >> 2) + 4 * lh + (v & 3);
+        float p = __builtin_amdgcn_exp2f(sacc[v] * sl2 - rm[v]);
+        if constexpr (decltype(masked)::value)
+          p = ((j < n) & (j <= n - bp + rv) & (rv < bp)) ? p : 0.f;
+        Pt[rv * LPITCH + lr] = p;
+        cs += p;
       }
     };
     if (edge) weights(std::true_type{});
@@ -305,40 +315,37 @@ __global__ __launch_bounds__(kThreads) void rep_lines(SelectArgs a) {
     // vertical lines: this lane's 16 rows, then the other lane half's (lower half first),
     // then the four waves in order after the barrier
     if (kt >= c0) {
-#pragma unroll
-      for (int b2 = 0; b2 < 2; ++b2) {
-        const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(cs[b2]),
-                                                         __float_as_uint(cs[b2]), false, false);
-        if (lh == 0) red[w][b2 * 32 + lr] = __uint_as_float(pr[0]) + __uint_as_float(pr[1]);
-      }
+      const auto pr =
+          __builtin_amdgcn_permlane32_swap(__float_as_uint(cs), __float_as_uint(cs), false, false);
+      if (lh == 0) red[w][lr] = __uint_as_float(pr[0]) + __uint_as_float(pr[1]);
     }
     __syncthreads();
     // slash lines: diagonal o with last-row key jl = n - 1 - o meets this tile for
-    // jl in [kt, kt + KT + bp - 1); rows r with key jl - (bp - 1) + r inside the tile
+    // jl in [kt, kt + LKT + bp - 1); rows r with key jl - (bp - 1) + r inside the tile
     const int jl = kt + tid;
-    if (tid < KT + bp - 1 && jl >= c0 && jl < c1) {
+    if (tid < LKT + bp - 1 && jl >= c0 && jl < c1) {
       const int rlo = max(0, bp - 1 - (jl - kt));
-      const int rhi = min(bp, bp - 1 - (jl - kt) + KT);
-      // element (rr, jl - (bp - 1) + rr - kt) of the tile: stride PT_PITCH + 1 along rr;
+      const int rhi = min(bp, bp - 1 - (jl - kt) + LKT);
+      // element (rr, jl - (bp - 1) + rr - kt) of the tile: stride LPITCH + 1 along rr;
       // eight partial sums keep eight LDS reads in flight (fixed order: deterministic)
-      const float *dp = Pt + (jl - (bp - 1) - kt) + rlo * (PT_PITCH + 1);
+      const float *dp = Pt + (jl - (bp - 1) - kt) + rlo * (LPITCH + 1);
       const int len = rhi - rlo;
       float d[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
       int i = 0;
       for (; i + 8 <= len; i += 8)
 #pragma unroll
-        for (int u = 0; u < 8; ++u) d[u] += dp[(i + u) * (PT_PITCH + 1)];
+        for (int u = 0; u < 8; ++u) d[u] += dp[(i + u) * (LPITCH + 1)];
 #pragma unroll
       for (int u = 0; u < 7; ++u)
-        if (i + u < len) d[u] += dp[(i + u) * (PT_PITCH + 1)];
+        if (i + u < len) d[u] += dp[(i + u) * (LPITCH + 1)];
       const float ds = ((d[0] + d[1]) + (d[2] + d[3])) + ((d[4] + d[5]) + (d[6] + d[7]));
       acc_s[jl - c0] += ds;
     }
     __syncthreads();
-    if (kt >= c0 && tid < KT) {
-      const int j = kt + tid;
-      if (j < c1)
-        a.a_v[(int64_t)h * a.total_tokens + tok0 + j] =
+    if (kt >= c0 && tid < LKT) {
+      const int jj = kt + tid;
+      if (jj < c1)
+        a.a_v[(int64_t)h * a.total_tokens + tok0 + jj] =
             ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
     }
   }
