@@ -775,6 +775,12 @@ __device__ __forceinline__ void sort_group_items(const SeqTable &st, const int32
   if (g == 0 && threadIdx.x < 8) queue[threadIdx.x] = 0;
   int np = 1;
   while (np < n_g) np <<= 1;
+  // each item's record is kept in LDS after the keys when both fit (it is read back by id
+  // after the sort instead of being fetched again); the list entries are read together,
+  // at indices clamped to the row's capacity I + 1
+  const int rec0 = (np + 1) & ~1;               // records start 16-byte aligned
+  const bool stash = (size_t)rec0 * 8 + (size_t)n_g * 16 <= (size_t)kSortItems * 8;
+  int4 *rec = reinterpret_cast<int4 *>(key + rec0);
   for (int id = threadIdx.x; id < np; id += blockDim.x) {
     unsigned long long kv = ~0ull;               // padding sorts last
     if (id < n_g) {
@@ -782,15 +788,21 @@ __device__ __forceinline__ void sort_group_items(const SeqTable &st, const int32
       const int s = seq_of_row(st, r);
       const int I = r - st.nb_off[s];
       const int h = g * G + kk;
-      const int cnt = max(0, min(kb_cnt[(int64_t)h * nb_total + r], I + 1));
       const int32_t *list = kb_idx + (int64_t)h * tri_total + st.tri_off[s] + (int64_t)I * (I + 1) / 2;
+      const int c_raw = kb_cnt[(int64_t)h * nb_total + r];
+      int32_t l[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) l[t] = list[min(t, I)];
+      const int cnt = max(0, min(c_raw, I + 1));
       unsigned long long e[3];
 #pragma unroll
-      for (int t = 0; t < 3; ++t)
-        e[t] = cnt > t + 1 ? min((unsigned)list[t + 1], 0x1FFFu) : 0x1FFFu;
+      for (int t = 0; t < 3; ++t) e[t] = cnt > t + 1 ? min((unsigned)l[t + 1], 0x1FFFu) : 0x1FFFu;
       const unsigned long long bucket = (unsigned long long)min(cnt >> 2, 1023);
       kv = ((1023ull - bucket) << 53) | (e[0] << 40) | (e[1] << 27) | (e[2] << 14) |
            (unsigned long long)id;
+      if (stash)
+        rec[id] = make_int4((int)(((uint32_t)s << 26) | ((uint32_t)kk << 13) | (uint32_t)I), cnt,
+                            cnt > 0 ? l[0] : -1, cnt > 1 ? l[1] : -1);
     }
     key[id] = kv;
   }
@@ -814,10 +826,14 @@ __device__ __forceinline__ void sort_group_items(const SeqTable &st, const int32
   }
   for (int t = threadIdx.x; t < n_g; t += blockDim.x) {
     const int id = (int)(key[t] & 0x3FFF);
-    const int r = id / G, kk = id % G;
-    const int s = seq_of_row(st, r);
-    items[(int64_t)g * n_g + t] =
-        item_record(st, kb_idx, kb_cnt, nb_total, tri_total, G, g, s, kk, r - st.nb_off[s]);
+    if (stash) {
+      items[(int64_t)g * n_g + t] = rec[id];
+    } else {
+      const int r = id / G, kk = id % G;
+      const int s = seq_of_row(st, r);
+      items[(int64_t)g * n_g + t] =
+          item_record(st, kb_idx, kb_cnt, nb_total, tri_total, G, g, s, kk, r - st.nb_off[s]);
+    }
   }
 }
 
