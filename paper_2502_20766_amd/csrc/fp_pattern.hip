@@ -226,6 +226,7 @@ __global__ __launch_bounds__(kThreads) void qa_logits(SelectArgs a) {
 }
 
 // Row softmax over J <= I of the flattened logits, one wave per row (in place).
+constexpr int kRowRegs = 16;   // rows up to 1024 blocks are held in registers
 __global__ __launch_bounds__(kThreads) void qa_softmax(SelectArgs a) {
   const int h = blockIdx.y;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -235,6 +236,32 @@ __global__ __launch_bounds__(kThreads) void qa_softmax(SelectArgs a) {
   if (a.pattern[s * a.hq + h] != FP_PATTERN_QUERY_AWARE) return;
   const int I = row - a.st.nb_off[s];
   float *x = a.flat + (int64_t)h * a.tri_total + a.st.tri_off[s] + (int64_t)I * (I + 1) / 2;
+  if (I < 64 * kRowRegs) {
+    // the row fits in registers: one read, one write (same operations in the same order as
+    // the streaming form below)
+    float xv[kRowRegs];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kRowRegs; ++u) {
+      const int J = lane + 64 * u;
+      xv[u] = J <= I ? x[J] : -INFINITY;
+      mx = fmaxf(mx, xv[u]);
+    }
+    for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    float se = 0.f;
+#pragma unroll
+    for (int u = 0; u < kRowRegs; ++u)
+      if (lane + 64 * u <= I) {
+        xv[u] = expf(xv[u] - mx);
+        se += xv[u];
+      }
+    for (int off = 32; off > 0; off >>= 1) se += __shfl_xor(se, off);
+    const float inv = 1.f / se;
+#pragma unroll
+    for (int u = 0; u < kRowRegs; ++u)
+      if (lane + 64 * u <= I) x[lane + 64 * u] = xv[u] * inv;
+    return;
+  }
   float mx = -INFINITY;
   for (int J = lane; J <= I; J += 64) mx = fmaxf(mx, x[J]);
   for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
