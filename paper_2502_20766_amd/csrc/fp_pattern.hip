@@ -164,13 +164,17 @@ constexpr int QT = 64;   // rows and columns of A_bar per workgroup tile
 
 // Tile (TI, TJ), TJ <= TI, of the logits scale * Q_bar_I . K_bar_J written into the
 // flattened causal layout.  Grid x enumerates the causal tile pairs of all sequences.
-// Each wave computes one 32x32 quarter with the fp32 MFMA (products and sums in fp32,
-// as the vector code would): lane (l % 32, l / 32) supplies Q_bar row l % 32 and
-// K_bar row l % 32 over dimensions [l / 32 * D / 2, +D / 2), so the reduction runs over
-// the same dimensions for both operands, read straight from global memory (L2-resident).
+// The tile's 64 Q_bar rows and 64 K_bar rows are staged in LDS with coalesced 16-byte
+// loads; each wave then computes one 32x32 quarter with the fp32 MFMA (products and sums
+// in fp32, as the vector code would): lane (l % 32, l / 32) supplies Q_bar row l % 32 and
+// K_bar row l % 32 over dimensions [l / 32 * D / 2, +D / 2), so the reduction runs over the
+// same dimensions for both operands.
 template <int D>
 __global__ __launch_bounds__(kThreads) void qa_logits(SelectArgs a) {
   typedef float f32x16 __attribute__((ext_vector_type(16)));
+  constexpr int P = D + 4;               // LDS row pitch in floats (16-byte rows, no conflicts)
+  __shared__ __attribute__((aligned(16))) float Qs[QT * P];
+  __shared__ __attribute__((aligned(16))) float Ks[QT * P];
   const int h = blockIdx.y;
   // locate sequence and tile pair
   int t = blockIdx.x, s = 0, nt = 0;
@@ -191,29 +195,31 @@ __global__ __launch_bounds__(kThreads) void qa_logits(SelectArgs a) {
   const int G = a.hq / a.hkv;
   const int g = h / G;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, lr = lane & 31, lh = lane >> 5;
-  const int I0 = TI * QT + 32 * (w >> 1), J0 = TJ * QT + 32 * (w & 1);
+  // stage the rows (rows past the sequence's last block are clamped; their logits are not
+  // written)
+  for (int i = tid; i < QT * (D / 4); i += kThreads) {
+    const int row = i / (D / 4), c = i % (D / 4);
+    const int I = min(TI * QT + row, nb - 1), J = min(TJ * QT + row, nb - 1);
+    *reinterpret_cast<float4 *>(Qs + row * P + 4 * c) = reinterpret_cast<const float4 *>(
+        a.qbar + ((int64_t)(a.st.nb_off[s] + I) * a.hq + h) * D)[c];
+    *reinterpret_cast<float4 *>(Ks + row * P + 4 * c) = reinterpret_cast<const float4 *>(
+        a.kbar + ((int64_t)(a.st.nb_off[s] + J) * a.hkv + g) * D)[c];
+  }
+  __syncthreads();
+  const int i0 = 32 * (w >> 1), j0 = 32 * (w & 1);          // quarter within the tile
+  const int I0 = TI * QT + i0, J0 = TJ * QT + j0;
   if (J0 > I0 + 31 || I0 >= nb) return;      // quarter above the diagonal or past the end
-  const int Ir = min(I0 + lr, nb - 1), Jr = min(J0 + lr, nb - 1);
-  const float4 *qp = reinterpret_cast<const float4 *>(
-      a.qbar + ((int64_t)(a.st.nb_off[s] + Ir) * a.hq + h) * D + lh * (D / 2));
-  const float4 *kp = reinterpret_cast<const float4 *>(
-      a.kbar + ((int64_t)(a.st.nb_off[s] + Jr) * a.hkv + g) * D + lh * (D / 2));
+  const float *qa = Qs + (i0 + lr) * P + lh * (D / 2);
+  const float *kb = Ks + (j0 + lr) * P + lh * (D / 2);
   f32x16 acc = {};
 #pragma unroll
-  for (int c = 0; c < D / 8; c += 4) {
-    float4 qv[4], kv[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      qv[u] = qp[c + u];
-      kv[u] = kp[c + u];
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qv[u].x, kv[u].x, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qv[u].y, kv[u].y, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qv[u].z, kv[u].z, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qv[u].w, kv[u].w, acc, 0, 0, 0);
-    }
+  for (int c = 0; c < D / 2; c += 4) {
+    const float4 qv = *reinterpret_cast<const float4 *>(qa + c);
+    const float4 kv = *reinterpret_cast<const float4 *>(kb + c);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qv.x, kv.x, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qv.y, kv.y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qv.z, kv.z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qv.w, kv.w, acc, 0, 0, 0);
   }
   // lane holds column J0 + lr of rows I0 + 8 (v / 4) + 4 lh + v % 4
   float *flat = a.flat + (int64_t)h * a.tri_total + a.st.tri_off[s];
