@@ -383,12 +383,14 @@ __global__ __launch_bounds__(1024) void convert_tiles(SelectArgs a) {
       }
       return is_selected(S0, flat[tri_row + J], (int)(tri_row + J));
     };
+    // selected count, only as far as the minimum budget needs it (exact whenever it stays
+    // below the target, which is the only case that uses it)
+    const int target = min(m, I + 1);
     int count = 0;
-    for (int J0 = 0; J0 <= I; J0 += 64) {
+    for (int J0 = 0; J0 <= I && count < target; J0 += 64) {
       const int J = J0 + lane;
       count += __popcll(__ballot(J <= I && sel(J)));
     }
-    const int target = min(m, I + 1);
     int jmin = I;          // vertical-slash top-up: every unselected J in [jmin, I)
     int n_added = 0;       // query-aware top-up: added[w][0..n_added)
     if (count < target) {
