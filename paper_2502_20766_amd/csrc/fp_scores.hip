@@ -154,7 +154,9 @@ __global__ __launch_bounds__(kThreads * HG) void rep_stats(SelectArgs a) {
     if (kt + KT < c1) tile.load(kbase, kv_row, kt + KT, n, tid);   // overlaps this tile
     f32x16 sacc[2];
     tile_scores<D>(Ks, qf, lr, lh, sacc);
-    float mt = -INFINITY;
+    // tile max on the raw scores (the scale is positive and rounding is monotonic, so the
+    // scaled max is the max of the scaled scores); the scale is folded into the exponent
+    float mr = -INFINITY;
     // masking only in tiles that reach past the chunk, past the first row's position, or
     // in waves holding rows beyond b' (a wave-uniform test)
     const bool edge = kt + KT > c1 || kt + KT - 1 > n - bp + 32 * w || 32 * w + 31 >= bp;
@@ -164,28 +166,22 @@ __global__ __launch_bounds__(kThreads * HG) void rep_stats(SelectArgs a) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int j = kt + b2 * 32 + 8 * (v >> 2) + 4 * lh + (v & 3);
-          float x = sacc[b2][v] * sl2;
-          if (j >= c1 || j > irow || r >= bp) x = -INFINITY;
-          sacc[b2][v] = x;
-          mt = fmaxf(mt, x);
+          if (j >= c1 || j > irow || r >= bp) sacc[b2][v] = -INFINITY;
+          mr = fmaxf(mr, sacc[b2][v]);
         }
     } else {
 #pragma unroll
       for (int b2 = 0; b2 < 2; ++b2)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float x = sacc[b2][v] * sl2;
-          sacc[b2][v] = x;
-          mt = fmaxf(mt, x);
-        }
+        for (int v = 0; v < 16; ++v) mr = fmaxf(mr, sacc[b2][v]);
     }
-    const float mn = fmaxf(m, mt);
+    const float mn = fmaxf(m, mr * sl2);
     const float mu = (mn == -INFINITY) ? 0.f : mn;
     float acc = 0.f;
 #pragma unroll
     for (int b2 = 0; b2 < 2; ++b2)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc += __builtin_amdgcn_exp2f(sacc[b2][v] - mu);
+      for (int v = 0; v < 16; ++v) acc += __builtin_amdgcn_exp2f(fmaf(sacc[b2][v], sl2, -mu));
     l = l * __builtin_amdgcn_exp2f(m - mu) + acc;
     m = mn;
   }
