@@ -238,7 +238,7 @@ constexpr int LPITCH = LKT + 1;                // odd pitch: diagonal reads are 
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void rep_lines(
     SelectArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[LKT * D];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][LKT * D];   // double-buffered K tile
   __shared__ float Pt[128 * LPITCH];           // Â tile, [row][key]
   __shared__ float acc_s[kScoreChunk];         // owned slash offsets
   __shared__ float red[4][LKT];                // per wave: column sums of the tile
@@ -276,18 +276,20 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
 
   // keys [c0 - 128, c0) are recomputed for the diagonals owned by this chunk
   const int kstart = max(c0 - 128, 0);
+  // two barriers per tile: after the weights (the next K tile is then stored into the other
+  // buffer, whose last reader finished a tile ago) and after the diagonal pass
   KTile<D, kThreads, LKT> tile;
   tile.load(kbase, kv_row, kstart, n, tid);
+  tile.store(Ks[0], tid);
+  if (kstart + LKT < c1) tile.load(kbase, kv_row, kstart + LKT, n, tid);
+  __syncthreads();
+  int buf = 0;
   for (int kt = kstart; kt < c1; kt += LKT) {
-    __syncthreads();
-    tile.store(Ks, tid);
-    __syncthreads();
-    if (kt + LKT < c1) tile.load(kbase, kv_row, kt + LKT, n, tid);   // overlaps this tile
     f32x16 sacc = {};
 #pragma unroll
     for (int k = 0; k < D / 16; ++k) {
       const bf16x8 kf =
-          *reinterpret_cast<const bf16x8 *>(Ks + lr * D + k_swz<D>(2 * k + lh, lr) * 8);
+          *reinterpret_cast<const bf16x8 *>(Ks[buf] + lr * D + k_swz<D>(2 * k + lh, lr) * 8);
       sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[k], kf, sacc, 0, 0, 0);
     }
     // masking only in tiles that reach past the sequence or the first row's position, or
@@ -316,6 +318,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
       if (lh == 0) red[w][lr] = __uint_as_float(pr[0]) + __uint_as_float(pr[1]);
     }
     __syncthreads();
+    if (kt + LKT < c1) {
+      tile.store(Ks[buf ^ 1], tid);
+      if (kt + 2 * LKT < c1) tile.load(kbase, kv_row, kt + 2 * LKT, n, tid);   // next-next tile
+    }
     // slash lines: diagonal o with last-row key jl = n - 1 - o meets this tile for
     // jl in [kt, kt + LKT + bp - 1); rows r with key jl - (bp - 1) + r inside the tile
     const int jl = kt + tid;
@@ -337,15 +343,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
       const float ds = ((d[0] + d[1]) + (d[2] + d[3])) + ((d[4] + d[5]) + (d[6] + d[7]));
       acc_s[jl - c0] += ds;
     }
-    __syncthreads();
     if (kt >= c0 && tid < LKT) {
       const int jj = kt + tid;
       if (jj < c1)
         a.a_v[(int64_t)h * a.total_tokens + tok0 + jj] =
             ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
     }
+    __syncthreads();
+    buf ^= 1;
   }
-  __syncthreads();
   for (int i = tid; i < c1 - c0; i += kThreads) {
     const int jl = c0 + i;
     a.a_s[(int64_t)h * a.total_tokens + tok0 + (n - 1 - jl)] = acc_s[i];
