@@ -7,8 +7,9 @@
 //   a_s[o] = sum_r A_hat[r, i_r - o] / b'      (slash lines, offset o = i - j)
 // A_hat is never stored: pass 1 computes each row's max and sum of exp per chunk of
 // 1024 keys, a combine kernel merges the chunks, pass 2 recomputes the scores tile by
-// tile and reduces columns and diagonals in LDS.  Every sum is in a fixed order (no
-// float atomics), so results are bit-reproducible.  Each pass-2 workgroup owns the slash
+// tile, sums the columns in registers (one key per lane) and the diagonals through an LDS
+// tile.  Every sum is in a fixed order (no float atomics), so results are
+// bit-reproducible.  Each pass-2 workgroup owns the slash
 // offsets whose last-row key falls in its chunk and recomputes the 128 keys before the
 // chunk so that it sees those diagonals whole.
 //
@@ -25,8 +26,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kThreads = 256;
-constexpr int KT = 64;             // keys per tile
-constexpr int PT_PITCH = KT + 1;   // odd pitch: diagonal and column reads are conflict free
+constexpr int KT = 64;             // keys per tile of the statistics pass
 
 __device__ __forceinline__ int seq_of_chunk(const SeqTable &st, int c) {
   int s = 0;
