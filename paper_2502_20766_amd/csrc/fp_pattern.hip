@@ -160,17 +160,18 @@ __global__ __launch_bounds__(kThreads) void pattern_search(SelectArgs a) {
 
 // ---------------------------------------------------------------- Algorithm 4 estimate
 
-constexpr int QT = 64;   // rows and columns of A_bar per workgroup tile
+constexpr int QT = 128;  // rows and columns of A_bar per workgroup tile
+constexpr int kLogitThreads = 1024;   // 16 waves, one 32x32 block each
 
 // Tile (TI, TJ), TJ <= TI, of the logits scale * Q_bar_I . K_bar_J written into the
 // flattened causal layout.  Grid x enumerates the causal tile pairs of all sequences.
-// The tile's 64 Q_bar rows and 64 K_bar rows are staged in LDS with coalesced 16-byte
-// loads; each wave then computes one 32x32 quarter with the fp32 MFMA (products and sums
+// The tile's 128 Q_bar rows and 128 K_bar rows are staged in LDS with coalesced 16-byte
+// loads; each wave then computes one 32x32 block with the fp32 MFMA (products and sums
 // in fp32, as the vector code would): lane (l % 32, l / 32) supplies Q_bar row l % 32 and
 // K_bar row l % 32 over dimensions [l / 32 * D / 2, +D / 2), so the reduction runs over the
 // same dimensions for both operands.
 template <int D>
-__global__ __launch_bounds__(kThreads) void qa_logits(SelectArgs a) {
+__global__ __launch_bounds__(kLogitThreads) void qa_logits(SelectArgs a) {
   typedef float f32x16 __attribute__((ext_vector_type(16)));
   constexpr int P = D + 4;               // LDS row pitch in floats (16-byte rows, no conflicts)
   __shared__ __attribute__((aligned(16))) float Qs[QT * P];
@@ -197,7 +198,7 @@ __global__ __launch_bounds__(kThreads) void qa_logits(SelectArgs a) {
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, lr = lane & 31, lh = lane >> 5;
   // stage the rows (rows past the sequence's last block are clamped; their logits are not
   // written)
-  for (int i = tid; i < QT * (D / 4); i += kThreads) {
+  for (int i = tid; i < QT * (D / 4); i += kLogitThreads) {
     const int row = i / (D / 4), c = i % (D / 4);
     const int I = min(TI * QT + row, nb - 1), J = min(TJ * QT + row, nb - 1);
     *reinterpret_cast<float4 *>(Qs + row * P + 4 * c) = reinterpret_cast<const float4 *>(
@@ -206,9 +207,9 @@ __global__ __launch_bounds__(kThreads) void qa_logits(SelectArgs a) {
         a.kbar + ((int64_t)(a.st.nb_off[s] + J) * a.hkv + g) * D)[c];
   }
   __syncthreads();
-  const int i0 = 32 * (w >> 1), j0 = 32 * (w & 1);          // quarter within the tile
+  const int i0 = 32 * (w >> 2), j0 = 32 * (w & 3);          // block within the tile
   const int I0 = TI * QT + i0, J0 = TJ * QT + j0;
-  if (J0 > I0 + 31 || I0 >= nb) return;      // quarter above the diagonal or past the end
+  if (J0 > I0 + 31 || I0 >= nb) return;      // block above the diagonal or past the end
   const float *qa = Qs + (i0 + lr) * P + lh * (D / 2);
   const float *kb = Ks + (j0 + lr) * P + lh * (D / 2);
   f32x16 acc = {};
@@ -297,9 +298,9 @@ hipError_t launch_qa_estimate(const SelectArgs &a, hipStream_t stream) {
     pairs += nt * (nt + 1) / 2;
   }
   if (a.d == 128)
-    hipLaunchKernelGGL(qa_logits<128>, dim3(pairs, a.hq), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(qa_logits<128>, dim3(pairs, a.hq), dim3(kLogitThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL(qa_logits<64>, dim3(pairs, a.hq), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(qa_logits<64>, dim3(pairs, a.hq), dim3(kLogitThreads), 0, stream, a);
   hipLaunchKernelGGL(qa_softmax, dim3((a.nb_total + 3) / 4, a.hq), dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
