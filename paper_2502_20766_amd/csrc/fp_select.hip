@@ -314,13 +314,28 @@ __global__ __launch_bounds__(256) void vs_marks(SelectArgs a) {
   const float *as = a.a_s + (int64_t)h * a.total_tokens + tok0;
   const int j0 = blockIdx.y * kMarkSlice;
   const int j1 = min(j0 + kMarkSlice, n);
-  for (int j = j0 + threadIdx.x; j < j1; j += blockDim.x) {
-    if (is_selected(S0, av[j], j)) mk[4 * (j / b) + 0] = 1;
-    if (is_selected(S1, as[j], j)) {
-      const int dl = j / b, t = j % b;
-      mk[4 * dl + 1] = 1;
-      if (t < last_rows) mk[4 * dl + 2] = 1;
-      if (t > 0 && dl + 1 < nb) mk[4 * (dl + 1) + 3] = 1;
+  // four scores per thread are loaded before any mark is stored (a byte store may alias
+  // the scores, so the compiler would otherwise wait for each load in turn)
+  const int nt = blockDim.x;
+  for (int base = j0 + threadIdx.x; base < j1; base += 4 * nt) {
+    float xv[4], xs[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int j = base + u * nt;
+      xv[u] = j < j1 ? av[j] : 0.f;
+      xs[u] = j < j1 ? as[j] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int j = base + u * nt;
+      if (j >= j1) break;
+      if (is_selected(S0, xv[u], j)) mk[4 * (j / b) + 0] = 1;
+      if (is_selected(S1, xs[u], j)) {
+        const int dl = j / b, t = j % b;
+        mk[4 * dl + 1] = 1;
+        if (t < last_rows) mk[4 * dl + 2] = 1;
+        if (t > 0 && dl + 1 < nb) mk[4 * (dl + 1) + 3] = 1;
+      }
     }
   }
 }
