@@ -121,16 +121,28 @@ __global__ __launch_bounds__(256) void sel_hist(SelectArgs a) {
   constexpr int shift = PASS == 0 ? 21 : (PASS == 1 ? 10 : 0);
   constexpr uint32_t dmask = PASS == 2 ? 1023u : 2047u;
   const int end = min(start + kSlice, S.n);
-  for (int i = start + threadIdx.x; i < end; i += blockDim.x) {
-    const float x = pr.scores[i];
-    const uint32_t key = __float_as_uint(x);
-    bool match = true;
-    if (PASS == 1) match = (key >> 21) == (S.prefix >> 21);
-    if (PASS == 2) match = (key >> 10) == (S.prefix >> 10);
-    if (match) {
-      const uint32_t dg = (key >> shift) & dmask;
-      atomicAdd(&cnt[dg], 1u);
-      atomicAdd(&mass[dg], to_fx(x));
+  const int nt = blockDim.x;
+  // four scores per thread are loaded before their histogram updates
+  for (int base = start + threadIdx.x; base < end; base += 4 * nt) {
+    float xs[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = base + u * nt;
+      xs[u] = i < end ? pr.scores[i] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (base + u * nt >= end) break;
+      const float x = xs[u];
+      const uint32_t key = __float_as_uint(x);
+      bool match = true;
+      if (PASS == 1) match = (key >> 21) == (S.prefix >> 21);
+      if (PASS == 2) match = (key >> 10) == (S.prefix >> 10);
+      if (match) {
+        const uint32_t dg = (key >> shift) & dmask;
+        atomicAdd(&cnt[dg], 1u);
+        atomicAdd(&mass[dg], to_fx(x));
+      }
     }
   }
   __syncthreads();
