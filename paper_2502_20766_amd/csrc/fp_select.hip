@@ -541,137 +541,230 @@ __global__ __launch_bounds__(256) void pool_lines(SelectArgs a) {
 
 // Query-aware rows when the selection is per query block (qa_mode 1) or rows are capped
 // (max_budget > 0).  One workgroup per (query head, query block I): the row's pooled scores
-// A_bar[I, J], J <= I, are sorted in LDS by (score desc, J asc).  The gamma-selected units
-// of the row are then a prefix of that order in both modes (flattened: the head's radix
+// A_bar[I, J], J <= I, are sorted by (score desc, J asc).  The gamma-selected units of the
+// row are then a prefix of that order in both modes (flattened: the head's radix
 // threshold; per query block: the shortest prefix whose exact fixed-point mass reaches
 // ceil(gamma * row total)).  Blocks 0 and I are always kept; the other blocks are taken
 // along the same order: the selected prefix, raised to min(m, I+1) blocks in total by the
 // top-up and lowered to max_budget by the cap.
-constexpr int kRowThreads = 256;
+constexpr int kRowWavesMax = 8;
 
-__global__ __launch_bounds__(kRowThreads) void qa_rows(SelectArgs a, int np_max) {
-  // dynamic LDS sized by the longest row: key[np_max] then keep[np_max]
-  extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
-  unsigned long long *key = reinterpret_cast<unsigned long long *>(dyn);  // (~bits) << 32 | J
-  uint8_t *keep = dyn + (size_t)np_max * sizeof(unsigned long long);
-  __shared__ unsigned long long pref[kRowThreads];
-  __shared__ int s_pos0, s_posI, s_kcut;
-  __shared__ uint32_t wcnt[kRowThreads / 64];
-  const int h = blockIdx.y;
-  const int row = blockIdx.x;
+struct RowShared {
+  unsigned long long wsum[kRowWavesMax];
+  uint32_t wcnt[kRowWavesMax];
+  int pos0, posI, kcut;
+};
+
+__device__ __forceinline__ unsigned long long key_min(unsigned long long u,
+                                                      unsigned long long v) {
+  return v < u ? v : u;
+}
+__device__ __forceinline__ unsigned long long key_max(unsigned long long u,
+                                                      unsigned long long v) {
+  return v < u ? u : v;
+}
+
+// One compare-exchange stage (SIZE, STRIDE) of an ascending bitonic sort of NT*E keys,
+// thread t holding positions t*E .. t*E+E-1 in k[].  Strides below E pair keys of one
+// thread, strides below 64*E pair lanes of one wave, wider strides go through LDS.
+template <int NT, int E, int SIZE, int STRIDE>
+__device__ __forceinline__ void bitonic_stage(unsigned long long (&k)[E],
+                                              unsigned long long *lds, int tid) {
+  if constexpr (STRIDE < E) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      if ((e & STRIDE) == 0) {
+        const int f = e | STRIDE;
+        const bool up = ((tid * E + e) & SIZE) == 0;
+        const unsigned long long u = k[e], v = k[f];
+        const bool sw = up ? (u > v) : (u < v);
+        k[e] = sw ? v : u;
+        k[f] = sw ? u : v;
+      }
+    }
+  } else if constexpr (STRIDE < 64 * E) {
+    constexpr int LX = STRIDE / E;
+    const bool take_min = ((tid & LX) == 0) == (((tid * E) & SIZE) == 0);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const unsigned long long v = __shfl_xor(k[e], LX);
+      k[e] = take_min ? key_min(k[e], v) : key_max(k[e], v);
+    }
+  } else {
+    __syncthreads();                 // the previous LDS stage's reads are done
+#pragma unroll
+    for (int e = 0; e < E; ++e) lds[tid * E + e] = k[e];
+    __syncthreads();
+    const bool take_min = (((tid * E) & STRIDE) == 0) == (((tid * E) & SIZE) == 0);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const unsigned long long v = lds[(tid * E + e) ^ STRIDE];
+      k[e] = take_min ? key_min(k[e], v) : key_max(k[e], v);
+    }
+  }
+  if constexpr (STRIDE > 1) bitonic_stage<NT, E, SIZE, STRIDE / 2>(k, lds, tid);
+}
+
+template <int NT, int E, int SIZE>
+__device__ __forceinline__ void bitonic_sort(unsigned long long (&k)[E],
+                                             unsigned long long *lds, int tid) {
+  bitonic_stage<NT, E, SIZE, SIZE / 2>(k, lds, tid);
+  if constexpr (SIZE < NT * E) bitonic_sort<NT, E, SIZE * 2>(k, lds, tid);
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_incl_scan(T v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const T u = __shfl_up(v, off);
+    if (lane >= off) v += u;
+  }
+  return v;
+}
+
+// One row of NT*E >= I+1 sort slots (E a power of two).
+template <int NT, int E>
+__device__ void qa_row(const SelectArgs &a, unsigned long long *lds, uint8_t *keep,
+                       RowShared &sh, int s, int h, int I, int row) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  int s = 0;
-  while (s + 1 < a.st.n_seq && a.st.nb_off[s + 1] <= row) ++s;
-  if (a.pattern[s * a.hq + h] != FP_PATTERN_QUERY_AWARE) return;
-  const int I = row - a.st.nb_off[s];
   const int len = I + 1;
   const int64_t tri_row = (int64_t)I * (I + 1) / 2;
   const float *x = a.flat + (int64_t)h * a.tri_total + a.st.tri_off[s] + tri_row;
-  int np = 1;
-  while (np < len) np <<= 1;
-  for (int i = tid; i < np; i += kRowThreads) {
-    key[i] = i < len ? ((unsigned long long)(~__float_as_uint(x[i])) << 32) | (uint32_t)i
-                     : ~0ull;
-    if (i < len) keep[i] = 0;
+  unsigned long long k[E];                           // (~score bits) << 32 | J
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int i = tid * E + e;
+    k[e] = i < len ? ((unsigned long long)(~__float_as_uint(x[i])) << 32) | (uint32_t)i
+                   : ~0ull;
   }
-  if (tid == 0) s_kcut = len;
-  __syncthreads();
-  for (int size = 2; size <= np; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = tid; i < np; i += kRowThreads) {
-        const int j = i ^ stride;
-        if (j > i) {
-          const bool up = (i & size) == 0;
-          const unsigned long long u = key[i], v = key[j];
-          if (up ? (u > v) : (u < v)) {
-            key[i] = v;
-            key[j] = u;
-          }
-        }
-      }
-      __syncthreads();
+  if (tid == 0) sh.kcut = len;
+  bitonic_sort<NT, E, 2>(k, lds, tid);
+  auto score_of = [](unsigned long long key) { return __uint_as_float(~(uint32_t)(key >> 32)); };
+  auto id_of = [](unsigned long long key) { return (int)(key & 0xFFFFFFFFu); };
+  // positions of the forced blocks 0 and I in the order
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int p = tid * E + e;
+    if (p < len) {
+      const int J = id_of(k[e]);
+      if (J == 0) sh.pos0 = p;
+      if (J == I) sh.posI = p;
     }
   }
-  // thread t owns the sorted positions [t*per, (t+1)*per)
-  const int per = (len + kRowThreads - 1) / kRowThreads;
-  const int p_lo = min(tid * per, len), p_hi = min(p_lo + per, len);
-  auto score_at = [&](int p) { return __uint_as_float(~(uint32_t)(key[p] >> 32)); };
-  auto id_at = [&](int p) { return (int)(key[p] & 0xFFFFFFFFu); };
-  int K = len;                                       // gamma-selected units of the row
+  int K;                                             // gamma-selected units of the row
   if (a.qa_mode == 1) {
-    unsigned long long mine = 0;
-    for (int p = p_lo; p < p_hi; ++p) mine += to_fx(score_at(p));
-    pref[tid] = mine;
+    auto mass_at = [&](int e) {
+      return tid * E + e < len ? to_fx(score_of(k[e])) : 0ull;
+    };
+    unsigned long long mine = 0ull;
+#pragma unroll
+    for (int e = 0; e < E; ++e) mine += mass_at(e);
+    const unsigned long long incl = wave_incl_scan(mine, lane);
+    if (lane == 63) sh.wsum[w] = incl;
     __syncthreads();
-    for (int off = 1; off < kRowThreads; off <<= 1) {      // inclusive scan (integers)
-      const unsigned long long v = tid >= off ? pref[tid - off] : 0ull;
-      __syncthreads();
-      pref[tid] += v;
-      __syncthreads();
+    unsigned long long run = incl - mine, total = 0ull;
+#pragma unroll
+    for (int q = 0; q < NT / 64; ++q) {
+      if (q < w) run += sh.wsum[q];
+      total += sh.wsum[q];
     }
-    const unsigned long long total = pref[kRowThreads - 1];
     unsigned long long thr = (unsigned long long)ceil((double)a.gamma * (double)total);
     if (thr < 1ull) thr = 1ull;
     if (total > 0ull && thr <= total) {
-      unsigned long long run = pref[tid] - mine;
-      for (int p = p_lo; p < p_hi; ++p) {
-        run += to_fx(score_at(p));
-        if (run >= thr) {
-          atomicMin(&s_kcut, p + 1);
-          break;
-        }
+      int cut = len;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        run += mass_at(e);
+        if (cut == len && run >= thr) cut = tid * E + e + 1;
       }
+      if (cut < len) atomicMin(&sh.kcut, cut);
     }
     __syncthreads();
-    K = s_kcut;
+    K = sh.kcut;
     if (tid == 0) atomicAdd(&a.units[(s * a.hq + h) * 2], K);
   } else {
     const SelState S0 = a.sel[(s * a.hq + h) * 2];
     int c = 0;
-    for (int p = p_lo; p < p_hi; ++p) c += is_selected(S0, score_at(p), (int)(tri_row + id_at(p)));
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      if (tid * E + e < len)
+        c += is_selected(S0, score_of(k[e]), (int)(tri_row + id_of(k[e])));
     c = (int)__reduce_add_sync(~0ull, (unsigned)c);
-    if (lane == 0) wcnt[w] = (uint32_t)c;
+    if (lane == 0) sh.wcnt[w] = (uint32_t)c;
     __syncthreads();
     K = 0;
-    for (int q = 0; q < kRowThreads / 64; ++q) K += (int)wcnt[q];
+#pragma unroll
+    for (int q = 0; q < NT / 64; ++q) K += (int)sh.wcnt[q];
   }
-  // positions of the forced blocks 0 and I in the order
-  for (int p = p_lo; p < p_hi; ++p) {
-    const int J = id_at(p);
-    if (J == 0) s_pos0 = p;
-    if (J == I) s_posI = p;
-  }
-  __syncthreads();
-  const int pos0 = s_pos0, posI = s_posI;
+  const int pos0 = sh.pos0, posI = sh.posI;
   const int f = I == 0 ? 1 : 2;                       // forced blocks
   const int in_f = (pos0 < K) + (I > 0 && posI < K);
   int k_final = K - in_f;                             // other blocks, along the order
   k_final = max(k_final, min(a.min_budget, len) - f);
   if (a.max_budget > 0) k_final = min(k_final, a.max_budget - f);
-  for (int p = p_lo; p < p_hi; ++p) {
-    const int J = id_at(p);
-    const int rank = p - (pos0 < p) - (I > 0 && posI < p);   // position among the others
-    if (J == 0 || J == I || rank < k_final) keep[J] = 1;
+  // every J <= I sits at exactly one position p < len, so this writes all of keep[0..I]
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int p = tid * E + e;
+    if (p < len) {
+      const int J = id_of(k[e]);
+      const int rank = p - (pos0 < p) - (I > 0 && posI < p);   // position among the others
+      keep[J] = (J == 0 || J == I || rank < k_final) ? 1 : 0;
+    }
   }
   __syncthreads();
-  int32_t *out = a.kb_idx + (int64_t)h * a.tri_total + a.st.tri_off[s] + tri_row;
-  int running = 0;
-  for (int J0 = 0; J0 < len; J0 += kRowThreads) {
-    const int J = J0 + tid;
-    const bool fl = J < len && keep[J];
-    const unsigned long long bal = __ballot(fl);
-    if (lane == 0) wcnt[w] = (uint32_t)__popcll(bal);
-    __syncthreads();
-    int before = 0, chunk = 0;
-    for (int q = 0; q < kRowThreads / 64; ++q) {
-      if (q < w) before += (int)wcnt[q];
-      chunk += (int)wcnt[q];
+  // ascending compaction: thread t owns blocks t*E .. t*E+E-1
+  uint32_t bits = 0u;
+  int cnt = 0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int J = tid * E + e;
+    if (J < len && keep[J]) {
+      bits |= 1u << e;
+      ++cnt;
     }
-    if (fl) out[running + before + __popcll(bal & __lanemask_lt())] = J;
-    running += chunk;
-    __syncthreads();
   }
-  if (tid == 0) a.kb_cnt[(int64_t)h * a.nb_total + row] = running;
+  const int incl = wave_incl_scan(cnt, lane);
+  if (lane == 63) sh.wcnt[w] = (uint32_t)incl;
+  __syncthreads();
+  int base = incl - cnt, total = 0;
+#pragma unroll
+  for (int q = 0; q < NT / 64; ++q) {
+    if (q < w) base += (int)sh.wcnt[q];
+    total += (int)sh.wcnt[q];
+  }
+  int32_t *out = a.kb_idx + (int64_t)h * a.tri_total + a.st.tri_off[s] + tri_row;
+#pragma unroll
+  for (int e = 0; e < E; ++e)
+    if ((bits >> e) & 1u) out[base++] = tid * E + e;
+  if (tid == 0) a.kb_cnt[(int64_t)h * a.nb_total + row] = total;
+}
+
+// NT threads per row, EMAX = sort slots per thread for the longest row (NT*EMAX >= max_nb).
+template <int NT, int EMAX>
+__global__ __launch_bounds__(NT) void qa_rows(SelectArgs a) {
+  // dynamic LDS: NT*EMAX sort keys, then NT*EMAX keep flags
+  extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
+  unsigned long long *lds = reinterpret_cast<unsigned long long *>(dyn);
+  uint8_t *keep = dyn + (size_t)NT * EMAX * sizeof(unsigned long long);
+  __shared__ RowShared sh;
+  const int h = blockIdx.y;
+  const int row = blockIdx.x;
+  int s = 0;
+  while (s + 1 < a.st.n_seq && a.st.nb_off[s + 1] <= row) ++s;
+  if (a.pattern[s * a.hq + h] != FP_PATTERN_QUERY_AWARE) return;
+  const int I = row - a.st.nb_off[s];
+  if (I < NT) {
+    qa_row<NT, 1>(a, lds, keep, sh, s, h, I, row);
+  } else if (I < 2 * NT) {
+    if constexpr (EMAX >= 2) qa_row<NT, 2>(a, lds, keep, sh, s, h, I, row);
+  } else if (I < 4 * NT) {
+    if constexpr (EMAX >= 4) qa_row<NT, 4>(a, lds, keep, sh, s, h, I, row);
+  } else if (I < 8 * NT) {
+    if constexpr (EMAX >= 8) qa_row<NT, 8>(a, lds, keep, sh, s, h, I, row);
+  } else {
+    if constexpr (EMAX >= 16) qa_row<NT, 16>(a, lds, keep, sh, s, h, I, row);
+  }
 }
 
 // gamma >= 1: every causal key block, no search (full attention).
@@ -697,18 +790,29 @@ __global__ __launch_bounds__(256) void dense_lists(SelectArgs a) {
 
 }  // namespace
 
-hipError_t launch_qa_rows(const SelectArgs &a, hipStream_t stream) {
-  int np_max = 1;
-  while (np_max < a.st.max_nb) np_max <<= 1;
-  const size_t dyn = (size_t)np_max * (sizeof(unsigned long long) + 1);
-  if (dyn > 65536) {          // rows above 7281 blocks: allow the larger LDS allocation
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(qa_rows),
+template <int NT, int EMAX>
+hipError_t launch_qa_rows_e(const SelectArgs &a, hipStream_t stream) {
+  const size_t dyn = (size_t)NT * EMAX * (sizeof(unsigned long long) + 1);
+  if (dyn > 65536) {          // rows above 4096 blocks: allow the larger LDS allocation
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(qa_rows<NT, EMAX>),
                                              hipFuncAttributeMaxDynamicSharedMemorySize,
                                              (int)dyn);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(qa_rows, dim3(a.nb_total, a.hq), dim3(kRowThreads), dyn, stream, a, np_max);
+  hipLaunchKernelGGL((qa_rows<NT, EMAX>), dim3(a.nb_total, a.hq), dim3(NT), dyn, stream, a);
   return hipGetLastError();
+}
+
+hipError_t launch_qa_rows(const SelectArgs &a, hipStream_t stream) {
+  // row I holds I+1 <= max_nb keys in NT*E slots; at most 16 slots per thread keeps the
+  // keys in registers, so the longest rows take 512 threads
+  if (a.st.max_nb <= 256) return launch_qa_rows_e<256, 1>(a, stream);
+  if (a.st.max_nb <= 512) return launch_qa_rows_e<256, 2>(a, stream);
+  if (a.st.max_nb <= 1024) return launch_qa_rows_e<256, 4>(a, stream);
+  if (a.st.max_nb <= 2048) return launch_qa_rows_e<256, 8>(a, stream);
+  if (a.st.max_nb <= 4096) return launch_qa_rows_e<256, 16>(a, stream);
+  if (a.st.max_nb <= 8192) return launch_qa_rows_e<512, 16>(a, stream);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_dense_lists(const SelectArgs &a, hipStream_t stream) {
