@@ -30,23 +30,27 @@ CASES = [
 ]
 
 
-def _check_layer(name, spec, gamma):
+def _check_layer(name, spec, gamma, max_budget=0, qa_mode=0):
     import paper_2502_20766_amd as fpx
     log(f"[fullsize] {name}: seqlens={spec.seqlens} hq={spec.hq} hkv={spec.hkv} gamma={gamma} "
-        f"tau={spec.tau} m={spec.min_budget}")
+        f"tau={spec.tau} m={spec.min_budget} max_budget={max_budget} qa_mode={qa_mode}")
     with Timer("generate"):
         layer = synth.make_layer(spec)
     q, k, v = to_device(layer)
     with Timer("device select + attention"):
-        idx = fpx.select(q, k, layer.cu_seqlens, gamma, spec.tau, spec.min_budget)
+        idx = fpx.select(q, k, layer.cu_seqlens, gamma, spec.tau, spec.min_budget,
+                         max_budget=max_budget, qa_mode=qa_mode)
         o = fpx.sparse_attn(q, k, v, idx)
         torch.cuda.synchronize()
     g = dict(masks=fpx.masks_from_indices(idx), pattern=idx.pattern.cpu().numpy(),
              js=idx.js.cpu().numpy(), units=idx.units.cpu().numpy())
+    if max_budget:
+        assert int(idx.kb_cnt.max()) <= max_budget
     o_host = o.float().cpu().numpy()
     del q, k, v, o
     with Timer("oracle selection, all heads"):
-        st = compare_selection(layer, g, gamma, spec.tau, spec.min_budget)
+        st = compare_selection(layer, g, gamma, spec.tau, spec.min_budget,
+                               max_budget=max_budget, qa_mode=qa_mode)
     log(f"  {st}")
     with Timer("oracle sampled outputs"):
         mx, mean = compare_outputs(layer, o_host, g["masks"], rows_per_head=4)
@@ -90,3 +94,26 @@ def test_gamma_sweep_selection_reduced_varlen(gamma):
     mx, mean = compare_outputs(layer, o.float().cpu().numpy(), g["masks"], rows_per_head=3)
     log(f"  output max_abs {mx:.3e} mean_abs {mean:.3e}")
     assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
+
+
+LONG_ROW_CASES = [
+    # (log2 tokens, max_budget, qa_mode): 2048, 4096 and 8192 key blocks per row at most,
+    # i.e. 8 and 16 sort slots per thread of 256, and 16 per thread of 512
+    (18, 0, 1),
+    (19, 24, 1),
+    (20, 0, 1),
+    (20, 40, 0),
+]
+
+
+@pytest.mark.parametrize("case", LONG_ROW_CASES, ids=[f"n2^{c[0]}-cap{c[1]}-qa{c[2]}"
+                                                     for c in LONG_ROW_CASES])
+def test_long_rows_per_query_block_and_capped(case):
+    """Per-query-block selection and the per-row cap on rows of up to 8192 key blocks: a
+    vertical-slash and a query-aware head over one KV head, every block set checked against
+    the oracle, outputs on sampled query blocks."""
+    from synth.layers import LayerSpec
+    lg, max_budget, qa_mode = case
+    spec = LayerSpec(f"rows-2h-n{1 << lg}", (1 << lg,), 2, 1, 128, 128, ("vs", "qa"), 16, 0.95,
+                     0.1, 8, 20250228 + 11 + lg)
+    _check_layer(spec.name, spec, spec.gamma, max_budget=max_budget, qa_mode=qa_mode)
