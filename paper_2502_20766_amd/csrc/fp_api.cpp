@@ -106,6 +106,8 @@ size_t select_layout(const fp_shape *sh, const Dims &dm, char *base, fp::SelectA
   char *a_s = take(sizeof(float) * hq * dm.total_tokens);
   char *av_blk = take(sizeof(float) * hq * dm.nb_total);
   char *as_blk = take(sizeof(float) * hq * dm.nb_total);
+  char *pat_logit = take(sizeof(float) * hq * dm.nb_total);
+  char *pat_ahat = take(sizeof(double) * hq * dm.nb_total);
   char *vs_marks = take(4 * hq * dm.nb_total);
   char *flat = take(sizeof(float) * hq * dm.tri_total);
   char *sel = take(sizeof(fp::SelState) * problems);
@@ -120,6 +122,8 @@ size_t select_layout(const fp_shape *sh, const Dims &dm, char *base, fp::SelectA
     a->a_s = (float *)a_s;
     a->av_blk = (float *)av_blk;
     a->as_blk = (float *)as_blk;
+    a->pat_logit = (float *)pat_logit;
+    a->pat_ahat = (double *)pat_ahat;
     a->vs_marks = (uint8_t *)vs_marks;
     a->flat = (float *)flat;
     a->sel = (fp::SelState *)sel;

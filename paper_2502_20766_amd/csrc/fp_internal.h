@@ -48,6 +48,8 @@ struct SelectArgs {
   float *a_s;              // [Hq][T]
   float *av_blk;           // [Hq][NB] a_v summed per key block (block-pooled lines)
   float *as_blk;           // [Hq][NB] a_s summed per offset block
+  float *pat_logit;        // [Hq][NB] scale * q_bar . K_bar_J of the pattern search
+  double *pat_ahat;        // [Hq][NB] a_hat[J] = a_v summed per key block
   uint8_t *vs_marks;       // [Hq][NB][4] per key block / diagonal: column, diagonal (full
                            // rows), diagonal (partial last row), diagonal + 1
   float *flat;             // [Hq][TRI]

@@ -1,7 +1,7 @@
 // Sparse pattern search (Algorithm 2) and the query-aware block estimate (Algorithm 4,
 // first steps) for gfx950.
 //
-// pattern_search: per (sequence, query head)
+// pattern_parts + pattern_decide: per (sequence, query head)
 //   a_bar = softmax(scale * avgpool(Q_hat) . avgpool(K)^T)       over all key blocks
 //   a_hat = block sums of the vertical line scores a_v            (= sumpool of A_hat / b')
 //   D_JS  = sqrt((KL(a_bar || m) + KL(a_hat || m)) / 2), m = (a_bar + a_hat) / 2, natural log
@@ -54,20 +54,29 @@ __device__ __forceinline__ float block_max(float v, float *scratch) {
 
 // ---------------------------------------------------------------- Algorithm 2
 
+// Key blocks of one (sequence, head) are split over kPatSlices workgroups for the logits
+// and the block sums, which dominate the work; one workgroup per (sequence, head) then
+// reduces them.
+constexpr int kPatSlices = 16;
+
+// pattern_parts: grid (n_seq * kPatSlices, Hq).  Each workgroup pools Q_hat into q_bar,
+// then for its key blocks J writes the logit scale * q_bar . K_bar_J (fp32) and
+// a_hat[J] = sum of a_v over the block's tokens (double, token order).
 template <int D>
-__global__ __launch_bounds__(kThreads) void pattern_search(SelectArgs a) {
+__global__ __launch_bounds__(kThreads) void pattern_parts(SelectArgs a) {
   constexpr int CH = D / 8;                 // 16-byte chunks of a query row
   constexpr int PH = kThreads / CH;         // row phases of the Q_hat pooling
-  extern __shared__ float dyn[];            // [max_nb] logits
   __shared__ __attribute__((aligned(16))) float qbar[D];
   __shared__ float qpart[PH][D];
-  __shared__ float fscr[kThreads];
-  __shared__ double dscr[kThreads];
-  const int s = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+  const int s = blockIdx.x / kPatSlices, slice = blockIdx.x % kPatSlices;
+  const int h = blockIdx.y, tid = threadIdx.x;
   const int tok0 = a.st.cu[s];
   const int n = a.st.cu[s + 1] - tok0;
   const int bp = min(a.block, n);
   const int nb = a.st.nb_off[s + 1] - a.st.nb_off[s];
+  const int per = (nb + kPatSlices - 1) / kPatSlices;
+  const int J0 = slice * per, J1 = min(nb, J0 + per);
+  if (J0 >= J1) return;
   const int G = a.hq / a.hkv;
   const int g = h / G;
 
@@ -97,9 +106,9 @@ __global__ __launch_bounds__(kThreads) void pattern_search(SelectArgs a) {
     qbar[tid] = acc / (float)bp;
   }
   __syncthreads();
-  // logits over key blocks (one block per thread, its pooled key read as 16-byte vectors)
-  float mx = -INFINITY;
-  for (int J = tid; J < nb; J += kThreads) {
+  const float *av = a.a_v + (int64_t)h * a.total_tokens + tok0;
+  for (int J = J0 + tid; J < J1; J += kThreads) {
+    // logit: the pooled key read as 16-byte vectors
     const float4 *kb =
         reinterpret_cast<const float4 *>(a.kbar + ((int64_t)(a.st.nb_off[s] + J) * a.hkv + g) * D);
     float4 kv[D / 4];
@@ -115,20 +124,9 @@ __global__ __launch_bounds__(kThreads) void pattern_search(SelectArgs a) {
       dot = fmaf(qv.z, kv[i].z, dot);
       dot = fmaf(qv.w, kv[i].w, dot);
     }
-    const float x = dot * a.scale;
-    dyn[J] = x;
-    mx = fmaxf(mx, x);
-  }
-  mx = block_max(mx, fscr);
-  double se = 0.0;
-  for (int J = tid; J < nb; J += kThreads) se += (double)expf(dyn[J] - mx);
-  se = block_sum(se, dscr);
-  // JSD terms, double precision
-  double jsd = 0.0;
-  const float *av = a.a_v + (int64_t)h * a.total_tokens + tok0;
-  for (int J = tid; J < nb; J += kThreads) {
-    const double pb = (double)expf(dyn[J] - mx) / se;              // a_bar[J]
-    double ph = 0.0;                                                // a_hat[J]
+    a.pat_logit[(int64_t)h * a.nb_total + a.st.nb_off[s] + J] = dot * a.scale;
+    // a_hat[J]: the block's line scores in token order
+    double ph = 0.0;
     const int j0 = J * a.block, j1 = min(j0 + a.block, n);
     const float *ap = av + j0;
     int j = 0;
@@ -144,6 +142,35 @@ __global__ __launch_bounds__(kThreads) void pattern_search(SelectArgs a) {
       }
     }
     for (; j < j1 - j0; ++j) ph += (double)ap[j];
+    a.pat_ahat[(int64_t)h * a.nb_total + a.st.nb_off[s] + J] = ph;
+  }
+}
+
+// pattern_decide: grid (n_seq, Hq).  a_bar = softmax of the logits, D_JS against a_hat
+// (double, fixed reduction trees), pattern.
+__global__ __launch_bounds__(kThreads) void pattern_decide(SelectArgs a) {
+  extern __shared__ float dyn[];            // [max_nb] logits
+  __shared__ float fscr[kThreads];
+  __shared__ double dscr[kThreads];
+  const int s = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+  const int nb = a.st.nb_off[s + 1] - a.st.nb_off[s];
+  const float *lg = a.pat_logit + (int64_t)h * a.nb_total + a.st.nb_off[s];
+  const double *ah = a.pat_ahat + (int64_t)h * a.nb_total + a.st.nb_off[s];
+  float mx = -INFINITY;
+  for (int J = tid; J < nb; J += kThreads) {
+    const float x = lg[J];
+    dyn[J] = x;
+    mx = fmaxf(mx, x);
+  }
+  mx = block_max(mx, fscr);
+  double se = 0.0;
+  for (int J = tid; J < nb; J += kThreads) se += (double)expf(dyn[J] - mx);
+  se = block_sum(se, dscr);
+  // JSD terms, double precision
+  double jsd = 0.0;
+  for (int J = tid; J < nb; J += kThreads) {
+    const double pb = (double)expf(dyn[J] - mx) / se;              // a_bar[J]
+    const double ph = ah[J];                                        // a_hat[J]
     const double m = 0.5 * (pb + ph);
     if (pb > 0.0) jsd += 0.5 * pb * log(pb / m);
     if (ph > 0.0) jsd += 0.5 * ph * log(ph / m);
@@ -282,11 +309,13 @@ __global__ __launch_bounds__(kThreads) void qa_softmax(SelectArgs a) {
 }  // namespace
 
 hipError_t launch_pattern_search(const SelectArgs &a, hipStream_t stream) {
-  const size_t dyn = (size_t)a.st.max_nb * sizeof(float);
+  const dim3 parts(a.st.n_seq * kPatSlices, a.hq);
   if (a.d == 128)
-    hipLaunchKernelGGL(pattern_search<128>, dim3(a.st.n_seq, a.hq), dim3(kThreads), dyn, stream, a);
+    hipLaunchKernelGGL(pattern_parts<128>, parts, dim3(kThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL(pattern_search<64>, dim3(a.st.n_seq, a.hq), dim3(kThreads), dyn, stream, a);
+    hipLaunchKernelGGL(pattern_parts<64>, parts, dim3(kThreads), 0, stream, a);
+  const size_t dyn = (size_t)a.st.max_nb * sizeof(float);
+  hipLaunchKernelGGL(pattern_decide, dim3(a.st.n_seq, a.hq), dim3(kThreads), dyn, stream, a);
   return hipGetLastError();
 }
 
