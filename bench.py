@@ -74,7 +74,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-sdpa", action="store_true", help="skip the PyTorch SDPA dense timing")
-    ap.add_argument("--cpu-sample-heads", type=int, default=16)
+    ap.add_argument("--cpu-sample-heads", type=int, default=32)
     ap.add_argument("--cpu-sample-rows", type=int, default=32)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM counters)")
