@@ -442,14 +442,25 @@ __global__ __launch_bounds__(1024) void convert_tiles(SelectArgs a) {
         for (; n_added < need; ++n_added) {
           float best = -1.f;
           int bj = 0x7FFFFFFF;
-          for (int J0 = 0; J0 <= I; J0 += 64) {
-            const int J = J0 + lane;
-            if (J > I || sel(J)) continue;
-            bool taken = false;
-            for (int q = 0; q < n_added; ++q) taken |= (added[w][q] == J);
-            if (taken) continue;
-            const float x = flat[tri_row + J];
-            if (x > best || (x == best && J < bj)) { best = x; bj = J; }
+          // four 64-block chunks per step, their scores loaded before the first is tested
+          for (int J0 = 0; J0 <= I; J0 += 256) {
+            float xs[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int J = J0 + 64 * u + lane;
+              xs[u] = J <= I ? flat[tri_row + J] : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int J = J0 + 64 * u + lane;
+              if (J > I || J == 0 || J == I || is_selected(S0, xs[u], (int)(tri_row + J)))
+                continue;
+              bool taken = false;
+              for (int q = 0; q < n_added; ++q) taken |= (added[w][q] == J);
+              if (taken) continue;
+              const float x = xs[u];
+              if (x > best || (x == best && J < bj)) { best = x; bj = J; }
+            }
           }
           for (int off = 32; off > 0; off >>= 1) {
             const float ob = __shfl_xor(best, off);
@@ -497,12 +508,33 @@ __global__ __launch_bounds__(1024) void convert_tiles(SelectArgs a) {
     }
     int32_t *out = a.kb_idx + (int64_t)h * a.tri_total + a.st.tri_off[s] + tri_row;
     int running = 0;
-    for (int J0 = 0; J0 <= I; J0 += 64) {
-      const int J = J0 + lane;
-      const bool f = J <= I && kept(J) && (J == 0 || J == I || J >= jcap);
-      const unsigned long long bal = __ballot(f);
-      if (f) out[running + __popcll(bal & __lanemask_lt())] = J;
-      running += __popcll(bal);
+    // four 64-block chunks per step; a query-aware row's scores of all four are loaded
+    // before the first is tested
+    for (int J0 = 0; J0 <= I; J0 += 256) {
+      float xs[4] = {0.f, 0.f, 0.f, 0.f};
+      if (!vs) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int J = J0 + 64 * u + lane;
+          if (J <= I) xs[u] = flat[tri_row + J];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int J = J0 + 64 * u + lane;
+        bool f = false;
+        if (J <= I) {
+          bool k = (J == 0 || J == I) ? true
+                   : vs               ? sel(J)
+                                      : is_selected(S0, xs[u], (int)(tri_row + J));
+          k = k || (J >= jmin && J < I);
+          for (int q = 0; q < n_added; ++q) k |= (added[w][q] == J);
+          f = k && (J == 0 || J == I || J >= jcap);
+        }
+        const unsigned long long bal = __ballot(f);
+        if (f) out[running + __popcll(bal & __lanemask_lt())] = J;
+        running += __popcll(bal);
+      }
     }
     if (lane == 0) a.kb_cnt[(int64_t)h * a.nb_total + a.st.nb_off[s] + I] = running;
   }
@@ -850,9 +882,11 @@ hipError_t launch_select_pipeline(const SelectArgs &a, hipStream_t stream) {
     const int mark_slices = a.vs_granularity == 1 ? (a.st.max_nb + 255) / 256
                                                   : (max_n + kMarkSlice - 1) / kMarkSlice;
     hipLaunchKernelGGL(vs_marks, dim3(a.st.n_seq * a.hq, mark_slices), dim3(256), 0, stream, a);
-    // row slices: about two workgroups per CU over all (sequence, head) pairs
+    // row slices: about two workgroups per CU over all (sequence, head) pairs, and at
+    // most four rows per wave on the longest sequence (packed batches mix lengths, and
+    // the workgroups of short sequences end early)
     const int pairs = a.st.n_seq * a.hq;
-    int slices = (512 + pairs - 1) / pairs;
+    int slices = max((512 + pairs - 1) / pairs, (a.st.max_nb + 63) / 64);
     slices = max(1, min(slices, (a.st.max_nb + 15) / 16));
     hipLaunchKernelGGL(convert_tiles, dim3(pairs, slices), dim3(1024), 0, stream, a);
   }
