@@ -26,6 +26,7 @@
 #include <type_traits>
 
 #include "fp_internal.h"
+#include "fp_sort.h"
 
 namespace fp {
 namespace {
@@ -758,6 +759,23 @@ __global__ void build_item_order_plain(SeqTable st, const int32_t *kb_idx, const
 }
 
 constexpr int kSortItems = 16384;   // items per KV group sorted in LDS (128 KB of keys)
+constexpr int kSortThreads = 1024;  // threads of a sorting workgroup
+
+// The kSortThreads * E keys in key[] sorted ascending in place: each thread takes E
+// consecutive keys into registers, the bitonic network exchanges them inside the thread,
+// across lanes, and through key[] for strides that cross waves.
+template <int E>
+__device__ __forceinline__ void sort_slots(unsigned long long *key) {
+  const int tid = threadIdx.x;
+  unsigned long long k[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) k[e] = key[tid * E + e];
+  bitonic_sort<kSortThreads, E>(k, key, tid);
+  __syncthreads();                       // the network's last reads of key[] are done
+#pragma unroll
+  for (int e = 0; e < E; ++e) key[tid * E + e] = k[e];
+  __syncthreads();
+}
 
 // Locality order of one KV group's items (s, head, I): ascending by
 //   [1023 - min(blocks / 4, 1023)] [first three listed blocks after block 0] [item id],
@@ -773,12 +791,13 @@ __device__ __forceinline__ void sort_group_items(const SeqTable &st, const int32
   const int nb_total = st.nb_off[st.n_seq];
   const int n_g = G * nb_total;
   if (g == 0 && threadIdx.x < 8) queue[threadIdx.x] = 0;
-  int np = 1;
+  // sort slots: a power of two, at least one per thread
+  int np = kSortThreads;
   while (np < n_g) np <<= 1;
   // each item's record is kept in LDS after the keys when both fit (it is read back by id
   // after the sort instead of being fetched again); the list entries are read together,
   // at indices clamped to the row's capacity I + 1
-  const int rec0 = (np + 1) & ~1;               // records start 16-byte aligned
+  const int rec0 = np;                          // records start 16-byte aligned
   const bool stash = (size_t)rec0 * 8 + (size_t)n_g * 16 <= (size_t)kSortItems * 8;
   int4 *rec = reinterpret_cast<int4 *>(key + rec0);
   for (int id = threadIdx.x; id < np; id += blockDim.x) {
@@ -807,22 +826,13 @@ __device__ __forceinline__ void sort_group_items(const SeqTable &st, const int32
     key[id] = kv;
   }
   __syncthreads();
-  // bitonic sort, ascending
-  for (int size = 2; size <= np; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = threadIdx.x; i < np; i += blockDim.x) {
-        const int j = i ^ stride;
-        if (j > i) {
-          const bool up = (i & size) == 0;
-          const unsigned long long x = key[i], y = key[j];
-          if (up ? (x > y) : (x < y)) {
-            key[i] = y;
-            key[j] = x;
-          }
-        }
-      }
-      __syncthreads();
-    }
+  // bitonic sort, ascending, np / kSortThreads keys per thread held in registers
+  switch (np / kSortThreads) {
+    case 1: sort_slots<1>(key); break;
+    case 2: sort_slots<2>(key); break;
+    case 4: sort_slots<4>(key); break;
+    case 8: sort_slots<8>(key); break;
+    default: sort_slots<16>(key); break;
   }
   for (int t = threadIdx.x; t < n_g; t += blockDim.x) {
     const int id = (int)(key[t] & 0x3FFF);

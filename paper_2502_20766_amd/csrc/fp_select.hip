@@ -26,6 +26,7 @@
 // and offset blocks of lines (pool_lines), and a selected unit marks the tiles of all its
 // lines.
 #include "fp_internal.h"
+#include "fp_sort.h"
 
 namespace fp {
 
@@ -586,63 +587,6 @@ struct RowShared {
   uint32_t wcnt[kRowWavesMax];
   int pos0, posI, kcut;
 };
-
-__device__ __forceinline__ unsigned long long key_min(unsigned long long u,
-                                                      unsigned long long v) {
-  return v < u ? v : u;
-}
-__device__ __forceinline__ unsigned long long key_max(unsigned long long u,
-                                                      unsigned long long v) {
-  return v < u ? u : v;
-}
-
-// One compare-exchange stage (SIZE, STRIDE) of an ascending bitonic sort of NT*E keys,
-// thread t holding positions t*E .. t*E+E-1 in k[].  Strides below E pair keys of one
-// thread, strides below 64*E pair lanes of one wave, wider strides go through LDS.
-template <int NT, int E, int SIZE, int STRIDE>
-__device__ __forceinline__ void bitonic_stage(unsigned long long (&k)[E],
-                                              unsigned long long *lds, int tid) {
-  if constexpr (STRIDE < E) {
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      if ((e & STRIDE) == 0) {
-        const int f = e | STRIDE;
-        const bool up = ((tid * E + e) & SIZE) == 0;
-        const unsigned long long u = k[e], v = k[f];
-        const bool sw = up ? (u > v) : (u < v);
-        k[e] = sw ? v : u;
-        k[f] = sw ? u : v;
-      }
-    }
-  } else if constexpr (STRIDE < 64 * E) {
-    constexpr int LX = STRIDE / E;
-    const bool take_min = ((tid & LX) == 0) == (((tid * E) & SIZE) == 0);
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const unsigned long long v = __shfl_xor(k[e], LX);
-      k[e] = take_min ? key_min(k[e], v) : key_max(k[e], v);
-    }
-  } else {
-    __syncthreads();                 // the previous LDS stage's reads are done
-#pragma unroll
-    for (int e = 0; e < E; ++e) lds[tid * E + e] = k[e];
-    __syncthreads();
-    const bool take_min = (((tid * E) & STRIDE) == 0) == (((tid * E) & SIZE) == 0);
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const unsigned long long v = lds[(tid * E + e) ^ STRIDE];
-      k[e] = take_min ? key_min(k[e], v) : key_max(k[e], v);
-    }
-  }
-  if constexpr (STRIDE > 1) bitonic_stage<NT, E, SIZE, STRIDE / 2>(k, lds, tid);
-}
-
-template <int NT, int E, int SIZE>
-__device__ __forceinline__ void bitonic_sort(unsigned long long (&k)[E],
-                                             unsigned long long *lds, int tid) {
-  bitonic_stage<NT, E, SIZE, SIZE / 2>(k, lds, tid);
-  if constexpr (SIZE < NT * E) bitonic_sort<NT, E, SIZE * 2>(k, lds, tid);
-}
 
 template <typename T>
 __device__ __forceinline__ T wave_incl_scan(T v, int lane) {
