@@ -8,8 +8,8 @@ import pytest
 
 import oracle
 import synth
-from parity import (O_MAX_ABS, O_MEAN_ABS, Timer, compare_outputs, compare_selection, log,
-                          to_device)
+from parity import (O_MAX_ABS, O_MEAN_ABS, Timer, assert_relaxations_bounded, compare_outputs,
+                    compare_selection, log, to_device)
 
 pytestmark = pytest.mark.gpu
 
@@ -154,6 +154,7 @@ def test_select_and_attention_vs_oracle(case):
     with Timer("oracle selection"):
         st = compare_selection(layer, g, spec.gamma, spec.tau, spec.min_budget)
     log(f"  {st}")
+    assert_relaxations_bounded(st)
     mx, mean = compare_outputs(layer, g["o"], g["masks"], rows_per_head=6)
     log(f"  output max_abs {mx:.3e} mean_abs {mean:.3e}")
     assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
@@ -252,7 +253,7 @@ def test_query_wise_selection_and_max_budget_vs_oracle(case):
         st = compare_selection(layer, g, spec.gamma, spec.tau, min_budget,
                                max_budget=max_budget, qa_mode=qa_mode, vs_granularity=vsg)
     log(f"  {st}")
-    assert st["order_ties"] <= max(2, st["heads"])        # rare: float32 vs float64 ranks
+    assert_relaxations_bounded(st)
     mx, mean = compare_outputs(layer, g["o"], g["masks"], rows_per_head=4)
     log(f"  output max_abs {mx:.3e} mean_abs {mean:.3e}")
     assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
@@ -322,6 +323,7 @@ def test_block64_select_and_attention_vs_oracle(case):
     with Timer("oracle selection"):
         st = compare_selection(layer, g, spec.gamma, spec.tau, spec.min_budget)
     log(f"  {st}")
+    assert_relaxations_bounded(st)
     mx, mean = compare_outputs(layer, g["o"], g["masks"], rows_per_head=6)
     log(f"  output max_abs {mx:.3e} mean_abs {mean:.3e}")
     assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
