@@ -71,6 +71,10 @@ def parse():
                          "the Llama-shaped layer from 4k to 128k tokens over a gamma sweep "
                          "(and dense attention per length), write the table to OUT.json and "
                          "print a one-line summary")
+    ap.add_argument("--gammas", default=None, metavar="G1,G2,...",
+                    help="also time selection and attention of the workload at each of these "
+                         "gammas (a time-versus-density table in the JSON line); default: the "
+                         "workload's own gamma list, if it has one")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-sdpa", action="store_true", help="skip the PyTorch SDPA dense timing")
@@ -79,6 +83,81 @@ def parse():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for HBM counters)")
     return ap.parse_args()
+
+
+def run_metadata():
+    """Device, host CPU and BLAS configuration of this run."""
+    import platform
+    import torch
+    meta = {"device": None, "arch": None, "compute_units": None, "cpu_model": None,
+            "host_threads": len(os.sched_getaffinity(0)), "blas": None,
+            "torch": torch.__version__, "hip": getattr(torch.version, "hip", None),
+            "python": platform.python_version()}
+    try:
+        prop = torch.cuda.get_device_properties(0)
+        meta.update(device=prop.name, arch=getattr(prop, "gcnArchName", None),
+                    compute_units=prop.multi_processor_count)
+    except Exception:  # noqa: BLE001
+        pass
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    meta["cpu_model"] = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        meta["blas"] = [{k: i.get(k) for k in ("internal_api", "version", "num_threads",
+                                               "threading_layer", "architecture")}
+                        for i in threadpool_info() if i.get("user_api") == "blas"]
+    except Exception:  # noqa: BLE001
+        pass
+    return meta
+
+
+def sample_clocks(enqueue, seconds, per_call_ms):
+    """Shader clocks (MHz, one per XCD) and socket power (W) read with amd-smi while
+    `enqueue()` calls (about `seconds` of GPU work) are running; None without amd-smi."""
+    import subprocess
+    import torch
+    n = max(2, int(math.ceil(seconds * 1e3 / max(per_call_ms, 1e-3))))
+    for _ in range(n):
+        enqueue()
+    out = None
+    try:
+        time.sleep(0.2)
+        r = subprocess.run(["amd-smi", "metric", "-c", "-p", "--json"], capture_output=True,
+                           text=True, timeout=30)
+        if r.returncode == 0:
+            data = json.loads(r.stdout)
+            g = data["gpu_data"][0] if isinstance(data, dict) else data[0]
+            clk = g.get("clock", {})
+            gfx = [int(v["clk"]["value"]) for k, v in sorted(clk.items())
+                   if k.startswith("gfx_") and isinstance(v, dict)
+                   and isinstance(v.get("clk"), dict) and str(v["clk"].get("value")).isdigit()]
+            pw = g.get("power", {}).get("socket_power", {}).get("value")
+            out = {"gfx_mhz": gfx, "gfx_mhz_mean": round(sum(gfx) / len(gfx), 1) if gfx else None,
+                   "socket_power_w": pw, "calls_in_flight": n}
+    except Exception as e:  # noqa: BLE001
+        out = {"error": str(e)[:200]}
+    torch.cuda.synchronize()
+    return out
+
+
+def causal_exact_flop(idx, shape, d):
+    """4 d x the causal (i >= j) query-key pairs inside the listed tiles: every
+    off-diagonal tile counts all its pairs, the diagonal tile of a block of r queries
+    r (r + 1) / 2 (every row lists its diagonal block)."""
+    cnt = idx.kb_cnt.cpu().numpy().astype(np.int64)
+    b = shape.block
+    seqlens = shape.seqlens.astype(np.int64)
+    rows = np.concatenate([np.minimum(b, n - b * np.arange(-(-n // b))) for n in seqlens])
+    hq = shape.c.num_q_heads
+    cnt = cnt[:hq * rows.size].reshape(hq, rows.size)
+    pairs = np.where(cnt > 0, (cnt - 1) * rows[None, :] * b + rows * (rows + 1) // 2, 0)
+    return float(4 * d * pairs.sum())
 
 
 def time_loop(fn, steps, stream):
@@ -96,8 +175,9 @@ def time_loop(fn, steps, stream):
 def cpu_baseline(layer, spec, gamma, n_heads, n_rows, max_budget=0, qa_mode=0,
                  vs_granularity=0):
     """Oracle on host cores over a bounded sample of the same layer, scaled to ms/layer:
-    selection of `n_heads` whole heads, attention on `n_rows` random query-block rows of
-    each of them; per-head and per-row means are scaled to all heads and rows."""
+    for every packed sequence, the selection of about n_heads / batch whole heads and the
+    attention of `n_rows` random query-block rows of each of them; per-head and per-row
+    means of each sequence are scaled to all heads and rows of that sequence."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
@@ -107,38 +187,36 @@ def cpu_baseline(layer, spec, gamma, n_heads, n_rows, max_budget=0, qa_mode=0,
     hq, hkv, d, b = spec.hq, spec.hkv, spec.d, spec.block
     G = hq // hkv
     cu = layer.cu_seqlens
+    batch = len(cu) - 1
     scale = 1.0 / math.sqrt(d)
     rng = np.random.default_rng(0)
-    heads = list(range(min(n_heads, hq)))
-    t_sel, t_rows, rows_done = 0.0, 0.0, 0
-    total_rows = 0
-    for s in range(len(cu) - 1):
-        total_rows += -(-(int(cu[s + 1]) - int(cu[s])) // b)
-    for h in heads:
-        s = len(cu) - 2                       # the longest (last) sequence
+    per_seq = max(1, min(hq, n_heads // batch))
+    heads = [int(h) for h in np.linspace(0, hq - 1, per_seq).round()]
+    est_ms, work_s, rows_done = 0.0, 0.0, 0
+    for s in range(batch):
         t0, t1 = int(cu[s]), int(cu[s + 1])
-        qs, ks, vs = layer.q[t0:t1, h], layer.k[t0:t1, h // G], layer.v[t0:t1, h // G]
-        t = time.perf_counter()
-        r = oracle.select_head(qs, ks, b, gamma, spec.tau, spec.min_budget, scale,
-                               max_budget=max_budget, qa_mode=qa_mode,
-                               vs_granularity=vs_granularity)
-        t_sel += time.perf_counter() - t
-        nb = r["mask"].shape[0]
-        rows = rng.choice(nb, size=min(n_rows, nb), replace=False)
-        t = time.perf_counter()
-        oracle.sparse_attention_rows(qs, ks, vs, r["mask"], b, scale, rows)
-        t_rows += time.perf_counter() - t
-        rows_done += len(rows)
-    sel_per_head = t_sel / len(heads)
-    row_mean = t_rows / max(rows_done, 1)
-    est_ms = 1e3 * (hq * len(cu[:-1]) * sel_per_head * (1 if len(cu) == 2 else 1) +
-                    hq * total_rows * row_mean)
-    work_s = t_sel + t_rows
+        nb = -(-(t1 - t0) // b)
+        t_sel, t_rows, rows_s = 0.0, 0.0, 0
+        for h in heads:
+            qs, ks, vs = layer.q[t0:t1, h], layer.k[t0:t1, h // G], layer.v[t0:t1, h // G]
+            t = time.perf_counter()
+            r = oracle.select_head(qs, ks, b, gamma, spec.tau, spec.min_budget, scale,
+                                   max_budget=max_budget, qa_mode=qa_mode,
+                                   vs_granularity=vs_granularity)
+            t_sel += time.perf_counter() - t
+            rows = rng.choice(nb, size=min(n_rows, nb), replace=False)
+            t = time.perf_counter()
+            oracle.sparse_attention_rows(qs, ks, vs, r["mask"], b, scale, rows)
+            t_rows += time.perf_counter() - t
+            rows_s += len(rows)
+        est_ms += 1e3 * hq * (t_sel / len(heads) + nb * t_rows / max(rows_s, 1))
+        work_s += t_sel + t_rows
+        rows_done += rows_s
     return {"value": est_ms, "unit": "ms/layer", "cores": int(cores), "kind": "oracle",
-            "sample": (f"float64 numpy oracle: selection of {len(heads)} whole heads and "
-                       f"attention on {rows_done} random query-block rows of the longest "
-                       f"sequence ({work_s:.1f} s of CPU work), scaled to {hq} heads x "
-                       f"{total_rows} rows")}
+            "sample": (f"float64 numpy oracle: per sequence, selection of {len(heads)} whole "
+                       f"heads and attention on {n_rows} random query-block rows of each "
+                       f"({batch} sequence(s), {rows_done} rows, {work_s:.1f} s of CPU work), "
+                       f"scaled to {hq} heads and every row")}
 
 
 SWEEP_LENGTHS = (4096, 8192, 16384, 32768, 65536, 131072)
@@ -310,24 +388,67 @@ def main():
         log(f"[bench] dense (library, all blocks) {ms_dense_lib:.3f} ms")
         try:
             import torch.nn.functional as F
-            if len(seqlens) == 1 and not args.no_sdpa:
-                qt = q.transpose(0, 1).unsqueeze(0).contiguous()
-                kt = k.transpose(0, 1).unsqueeze(0).repeat_interleave(
-                    spec.hq // spec.hkv, dim=1).contiguous()
-                vt = v.transpose(0, 1).unsqueeze(0).repeat_interleave(
-                    spec.hq // spec.hkv, dim=1).contiguous()
-                with torch.nn.attention.sdpa_kernel([torch.nn.attention.SDPBackend.FLASH_ATTENTION]):
-                    F.scaled_dot_product_attention(qt, kt, vt, is_causal=True)
-                    ms_sdpa = time_loop(lambda: F.scaled_dot_product_attention(qt, kt, vt,
-                                                                               is_causal=True),
-                                        max(2, args.steps // 3), stream)
+            if not args.no_sdpa:
+                # one SDPA call per sequence (SDPA has no packed variable-length form); the
+                # dense time of a packed layer is the sum over its sequences
+                ms_sdpa = 0.0
+                for si in range(len(seqlens)):
+                    t0, t1 = int(cu[si]), int(cu[si + 1])
+                    qt = q[t0:t1].transpose(0, 1).unsqueeze(0).contiguous()
+                    kt = k[t0:t1].transpose(0, 1).unsqueeze(0).repeat_interleave(
+                        spec.hq // spec.hkv, dim=1).contiguous()
+                    vt = v[t0:t1].transpose(0, 1).unsqueeze(0).repeat_interleave(
+                        spec.hq // spec.hkv, dim=1).contiguous()
+                    with torch.nn.attention.sdpa_kernel(
+                            [torch.nn.attention.SDPBackend.FLASH_ATTENTION]):
+                        F.scaled_dot_product_attention(qt, kt, vt, is_causal=True)
+                        ms_sdpa += time_loop(
+                            lambda: F.scaled_dot_product_attention(qt, kt, vt, is_causal=True),
+                            max(2, args.steps // 3), stream)
+                    del qt, kt, vt
                 dense["torch_sdpa_flash_ms"] = ms_sdpa
+                if len(seqlens) > 1:
+                    dense["torch_sdpa_flash_note"] = "sum of one call per packed sequence"
                 log(f"[bench] dense (torch SDPA flash) {ms_sdpa:.3f} ms")
-                del qt, kt, vt
         except Exception as e:  # noqa: BLE001
             dense["torch_sdpa_error"] = str(e)[:200]
             log(f"[bench] torch SDPA unavailable: {e}")
     dense_ms = min([x for kk, x in dense.items() if kk.endswith("_ms")] or [float("nan")])
+    f_exact = causal_exact_flop(idx, shape, spec.d)
+    log("[bench] clocks under the attention kernel")
+    clocks = sample_clocks(do_attn, 1.5, ms_attn)
+
+    gamma_table = None
+    gammas = ([float(x) for x in args.gammas.split(",")] if args.gammas
+              else list(getattr(spec, "gammas", None) or []))
+    if gammas:
+        gamma_table = []
+        for gm in gammas:
+            pg = fpx.params(gm, spec.tau, spec.min_budget, **sel_kw)
+            ws_g = torch.empty(max(fpx.select_workspace_size(shape, pg), 1), dtype=torch.uint8,
+                               device=dev)
+            idx_g = fpx.empty_indices(shape, dev)
+
+            def sel_g():
+                fpx.select(q, k, cu, gm, spec.tau, spec.min_budget, block=spec.block, out=idx_g,
+                           workspace=ws_g, **sel_kw)
+
+            def att_g():
+                fpx.sparse_attn(q, k, v, idx_g, out=o, workspace=ws_att)
+            sel_g()
+            att_g()
+            ms_s = time_loop(sel_g, args.steps, stream)
+            ms_a = time_loop(att_g, args.steps, stream)
+            tiles_g = int(idx_g.kb_cnt.sum().item())
+            row = {"gamma": gm, "select_ms": round(ms_s, 4), "attn_ms": round(ms_a, 4),
+                   "layer_ms": round(ms_s + ms_a, 4), "density": round(tiles_g / causal_tiles, 5),
+                   "attn_tflops_on_computed_blocks": round(
+                       4 * spec.block ** 2 * spec.d * tiles_g / (ms_a * 1e-3) / 1e12, 2),
+                   "speedup_vs_dense": round(dense_ms / (ms_s + ms_a), 3) if dense else None}
+            gamma_table.append(row)
+            log(f"[bench] gamma {gm}: select {ms_s:.3f} attn {ms_a:.3f} ms, density "
+                f"{row['density']:.4f}")
+            del ws_g, idx_g
 
     result = {
         "metric": "sparse prefill ms/layer + effective TFLOP/s vs dense at 128k; % of MFMA peak",
@@ -362,8 +483,16 @@ def main():
                      "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": attn_traffic_bytes(spec.name),
                      "kernel": f"sparse_fa_fwd<{spec.d}, {spec.block}>",
-                     "per_launch_flop": f_comp},
+                     "per_launch_flop": f_comp,
+                     "per_launch_flop_causal_exact": f_exact,
+                     "timed": "whole fp_sparse_attn call (work-order set-up + attention "
+                              "kernel), hipEvents on the launch stream"},
+        "attn_tflops_causal_exact": round(f_exact / (ms_attn * 1e-3) / 1e12, 2),
+        "clocks_under_attention": clocks,
+        "run": run_metadata(),
     }
+    if gamma_table is not None:
+        result["gamma_table"] = gamma_table
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle, bounded sample)")
         result["cpu_baseline"] = cpu_baseline(layer, spec, gamma, args.cpu_sample_heads,

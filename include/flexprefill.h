@@ -104,6 +104,10 @@ typedef struct fp_indices {
   uint8_t *pattern;
   float *js;
   int32_t *units;
+  float softmax_scale;  /* HOST field: the scale the lists were selected with.  fp_select */
+                        /* writes the scale it used (params->softmax_scale, or 1/sqrt(d) */
+                        /* when that is 0); fp_sparse_attn attends with this scale (0 =>  */
+                        /* 1/sqrt(d)), so selection and attention share one scale.        */
 } fp_indices;
 
 /* Element counts of fp_indices.kb_idx and .kb_cnt for `shape`.  Host only. */
@@ -124,19 +128,21 @@ fp_status fp_validate(const fp_shape *shape, const fp_params *params, size_t ws_
 
 /* Pattern search + index selection (Algorithm 1 up to S; Algorithms 2-4).
  * q: [T][Hq][d] bf16, k: [T][Hkv][d] bf16 (device).  ws: device workspace of
- * ws_bytes >= fp_select_workspace_size().  Writes every field of *out. */
+ * ws_bytes >= fp_select_workspace_size().  Enqueues the writes of every device buffer of
+ * *out and sets out->softmax_scale on the host. */
 fp_status fp_select(const fp_shape *shape, const void *q, const void *k,
-                    const fp_params *params, const fp_indices *out, void *ws,
+                    const fp_params *params, fp_indices *out, void *ws,
                     size_t ws_bytes, void *stream);
 
 /* Block-sparse causal attention O = A(Q, K, V, S) (Section 2): query i of block I
- * attends to keys j <= i whose key block is listed in row (s, h, I) of idx.
+ * attends to keys j <= i whose key block is listed in row (s, h, I) of idx, with the
+ * softmax scale idx->softmax_scale (0 => 1/sqrt(d); finite, >= 0).
  * q, o: [T][Hq][d] bf16; k, v: [T][Hkv][d] bf16; idx->kb_idx, idx->kb_cnt as written by
- * fp_select (other idx fields unused).  Listed blocks outside [0, I] are skipped; a
- * query row with no visible key gets O = 0.  softmax_scale 0 => 1/sqrt(d). */
+ * fp_select (pattern, js and units unused).  Listed blocks outside [0, I] are skipped; a
+ * query row with no visible key gets O = 0. */
 fp_status fp_sparse_attn(const fp_shape *shape, const void *q, const void *k,
-                         const void *v, const fp_indices *idx, float softmax_scale,
-                         void *o, void *ws, size_t ws_bytes, void *stream);
+                         const void *v, const fp_indices *idx, void *o, void *ws,
+                         size_t ws_bytes, void *stream);
 
 /* Static description of a status code. */
 const char *fp_status_string(fp_status status);

@@ -14,7 +14,9 @@ from dataclasses import dataclass
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libflexprefill.so")
+# the in-tree build; FLEXPREFILL_LIB names another build of the same library (e.g. one with
+# the host code instrumented by AddressSanitizer)
+LIB_PATH = os.environ.get("FLEXPREFILL_LIB") or os.path.join(_PKG, "libflexprefill.so")
 
 FP_OK, FP_ERR_INVALID_ARG, FP_ERR_UNSUPPORTED, FP_ERR_WORKSPACE, FP_ERR_HIP = range(5)
 PATTERN_QUERY_AWARE, PATTERN_VERTICAL_SLASH, PATTERN_DENSE = 0, 1, 2
@@ -43,7 +45,8 @@ class FpParams(ctypes.Structure):
 
 class FpIndices(ctypes.Structure):
     _fields_ = [("kb_idx", ctypes.c_void_p), ("kb_cnt", ctypes.c_void_p),
-                ("pattern", ctypes.c_void_p), ("js", ctypes.c_void_p), ("units", ctypes.c_void_p)]
+                ("pattern", ctypes.c_void_p), ("js", ctypes.c_void_p), ("units", ctypes.c_void_p),
+                ("softmax_scale", ctypes.c_float)]
 
 
 _lib_handle = None
@@ -65,7 +68,7 @@ def lib() -> ctypes.CDLL:
         h.fp_attn_workspace_size.argtypes = [S, sz]
         h.fp_validate.argtypes = [S, P, ctypes.c_size_t]
         h.fp_select.argtypes = [S, vp, vp, P, X, vp, ctypes.c_size_t, vp]
-        h.fp_sparse_attn.argtypes = [S, vp, vp, vp, X, ctypes.c_float, vp, vp, ctypes.c_size_t, vp]
+        h.fp_sparse_attn.argtypes = [S, vp, vp, vp, X, vp, vp, ctypes.c_size_t, vp]
         h.fp_status_string.argtypes = [ctypes.c_int]
         h.fp_status_string.restype = ctypes.c_char_p
         h.fp_last_error.argtypes = []
@@ -138,17 +141,19 @@ def validate(shape: Shape, p: FpParams | None, ws_bytes: int) -> int:
 
 @dataclass
 class Indices:
-    """Device outputs of select(): torch tensors on the GPU."""
+    """Device outputs of select(): torch tensors on the GPU, plus the softmax scale the
+    lists were selected with (host float; 0 = 1/sqrt(d)), which sparse_attn attends with."""
     shape: Shape
     kb_idx: object      # int32 [Hq * TRI]
     kb_cnt: object      # int32 [Hq * NB]
     pattern: object     # uint8 [B * Hq]
     js: object          # float32 [B * Hq]
     units: object       # int32 [B * Hq * 2]
+    softmax_scale: float = 0.0
 
     def c(self) -> FpIndices:
         return FpIndices(self.kb_idx.data_ptr(), self.kb_cnt.data_ptr(), self.pattern.data_ptr(),
-                         self.js.data_ptr(), self.units.data_ptr())
+                         self.js.data_ptr(), self.units.data_ptr(), float(self.softmax_scale))
 
 
 def _stream_ptr(stream):
@@ -157,10 +162,34 @@ def _stream_ptr(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def _check_tensor(x, name, ndim):
+def _check_tensor(x, name, ndim, dtype=None):
     import torch
-    if not (x.is_cuda and x.dtype == torch.bfloat16 and x.dim() == ndim and x.is_contiguous()):
-        raise ValueError(f"{name} must be a contiguous bf16 CUDA tensor of {ndim} dims")
+    dtype = torch.bfloat16 if dtype is None else dtype
+    if not (x.is_cuda and x.dtype == dtype and x.dim() == ndim and x.is_contiguous()):
+        raise ValueError(f"{name} must be a contiguous {dtype} CUDA tensor of {ndim} dims")
+
+
+def check_shapes(shape: Shape, q=None, k=None, v=None, o=None, index_lens=None):
+    """Host-only check of one call's buffer shapes against the problem `shape`, before any
+    launch: the C ABI sees raw device pointers and cannot check buffer sizes itself.
+    q, k, v, o: shape tuples (or None); index_lens: element counts (kb_idx, kb_cnt,
+    pattern, js, units) of the index buffers (or None).  Requires q and o = (T, Hq, d),
+    k and v = (T, Hkv, d) with T = cu_seqlens[-1], and index buffers at least as long as
+    the problem needs.  Raises ValueError naming the first mismatch."""
+    T = int(shape.cu[-1])
+    hq, hkv, d = shape.c.num_q_heads, shape.c.num_kv_heads, shape.c.head_dim
+    want = {"q": (T, hq, d), "k": (T, hkv, d), "v": (T, hkv, d), "o": (T, hq, d)}
+    for name, got in (("q", q), ("k", k), ("v", v), ("o", o)):
+        if got is not None and tuple(int(x) for x in got) != want[name]:
+            raise ValueError(f"{name} has shape {tuple(got)}; the problem (T={T}, Hq={hq}, "
+                             f"Hkv={hkv}, d={d}) needs {want[name]}")
+    if index_lens is not None:
+        n_idx, n_cnt = indices_size(shape)
+        b = shape.c.batch
+        need = (max(n_idx, 1), max(n_cnt, 1), b * hq, b * hq, b * hq * 2)
+        for name, got, n in zip(("kb_idx", "kb_cnt", "pattern", "js", "units"), index_lens, need):
+            if got is not None and int(got) < n:
+                raise ValueError(f"{name} holds {got} elements; the problem needs {n}")
 
 
 def empty_indices(shape: Shape, device):
@@ -185,6 +214,7 @@ def select(q, k, cu_seqlens, gamma, tau, min_budget=8, block=128, softmax_scale=
     _check_tensor(q, "q", 3)
     _check_tensor(k, "k", 3)
     shape = Shape(cu_seqlens, q.shape[1], k.shape[1], q.shape[2], block)
+    check_shapes(shape, q=q.shape, k=k.shape)
     p = params(gamma, tau, min_budget, softmax_scale, force_pattern, max_budget, qa_mode,
                vs_granularity)
     ws_bytes = select_workspace_size(shape, p)
@@ -192,40 +222,55 @@ def select(q, k, cu_seqlens, gamma, tau, min_budget=8, block=128, softmax_scale=
         workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
     if out is None:
         out = empty_indices(shape, q.device)
+    _check_indices(out, shape)
     oc = out.c()
     _check(lib().fp_select(ctypes.byref(shape.c), ctypes.c_void_p(q.data_ptr()),
                            ctypes.c_void_p(k.data_ptr()), ctypes.byref(p), ctypes.byref(oc),
                            ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
                            _stream_ptr(stream)), "fp_select")
+    out.shape = shape
+    out.softmax_scale = float(oc.softmax_scale)
     return out
 
 
-def sparse_attn(q, k, v, indices: Indices, softmax_scale=0.0, out=None, workspace=None,
-                stream=None):
-    """O = A(Q, K, V, S) over the key-block lists in `indices`."""
+def _check_indices(ind: Indices, shape: Shape):
+    import torch
+    for name, x, dt in (("kb_idx", ind.kb_idx, torch.int32), ("kb_cnt", ind.kb_cnt, torch.int32),
+                        ("pattern", ind.pattern, torch.uint8), ("js", ind.js, torch.float32),
+                        ("units", ind.units, torch.int32)):
+        _check_tensor(x, name, 1, dt)
+    check_shapes(shape, index_lens=(ind.kb_idx.numel(), ind.kb_cnt.numel(), ind.pattern.numel(),
+                                    ind.js.numel(), ind.units.numel()))
+
+
+def sparse_attn(q, k, v, indices: Indices, out=None, workspace=None, stream=None):
+    """O = A(Q, K, V, S) over the key-block lists in `indices`, with the softmax scale the
+    lists were selected with (indices.softmax_scale)."""
     import torch
     for name, x in (("q", q), ("k", k), ("v", v)):
         _check_tensor(x, name, 3)
     shape = indices.shape
+    if out is None:
+        out = torch.empty_like(q)
+    _check_tensor(out, "out", 3)
+    check_shapes(shape, q=q.shape, k=k.shape, v=v.shape, o=out.shape)
+    _check_indices(indices, shape)
     ws_bytes = attn_workspace_size(shape)
     if workspace is None:
         workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
-    if out is None:
-        out = torch.empty_like(q)
     ic = indices.c()
     _check(lib().fp_sparse_attn(ctypes.byref(shape.c), ctypes.c_void_p(q.data_ptr()),
                                 ctypes.c_void_p(k.data_ptr()), ctypes.c_void_p(v.data_ptr()),
-                                ctypes.byref(ic), float(softmax_scale),
-                                ctypes.c_void_p(out.data_ptr()),
+                                ctypes.byref(ic), ctypes.c_void_p(out.data_ptr()),
                                 ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
                                 _stream_ptr(stream)), "fp_sparse_attn")
     return out
 
 
-def indices_from_masks(shape: Shape, masks, device):
+def indices_from_masks(shape: Shape, masks, device, softmax_scale=0.0):
     """Pack host block masks {(s, h): bool [nb, nb]} into the kb_idx / kb_cnt layout
-    (ascending key blocks per row).  Host-side data marshalling for callers that bring
-    their own index sets."""
+    (ascending key blocks per row), to be attended with `softmax_scale` (0 = 1/sqrt(d)).
+    Host-side data marshalling for callers that bring their own index sets."""
     import torch
     n_idx, n_cnt = indices_size(shape)
     hq = shape.c.num_q_heads
@@ -246,7 +291,8 @@ def indices_from_masks(shape: Shape, masks, device):
     return Indices(shape, torch.from_numpy(kb_idx).to(device), torch.from_numpy(kb_cnt).to(device),
                    torch.zeros(b * hq, dtype=torch.uint8, device=device),
                    torch.zeros(b * hq, dtype=torch.float32, device=device),
-                   torch.zeros(b * hq * 2, dtype=torch.int32, device=device))
+                   torch.zeros(b * hq * 2, dtype=torch.int32, device=device),
+                   float(softmax_scale))
 
 
 def masks_from_indices(indices: Indices):

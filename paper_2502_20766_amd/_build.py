@@ -17,7 +17,8 @@ OBJ_DIR = os.path.join(PKG, "_build")
 SOURCES = ["fp_attn.hip", "fp_scores.hip", "fp_pattern.hip", "fp_select.hip", "fp_api.cpp"]
 ARCH = "gfx950"
 # Packed fp32 instructions are disabled for every device compilation.
-FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
+# Warnings are errors on both the host and the device pass.
+FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Werror",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 

@@ -71,13 +71,18 @@ fp_status check_shape(const fp_shape *sh, Dims *dm) {
   return FP_OK;
 }
 
+// A softmax scale argument: finite and >= 0 (0 selects 1 / sqrt(d)).
+bool scale_ok(float s) { return s >= 0.f && !isnan(s) && !isinf(s); }
+float resolved_scale(float s, int head_dim) {
+  return s > 0.f ? s : 1.0f / sqrtf((float)head_dim);
+}
+
 fp_status check_params(const fp_shape *sh, const fp_params *p) {
   if (!(p->gamma > 0.f) || !(p->gamma <= 1.f) || isnan(p->gamma)) return FP_ERR_INVALID_ARG;
   if (!(p->tau >= 0.f) || !(p->tau <= 1.f)) return FP_ERR_INVALID_ARG;
   if (p->min_budget_blocks < 0) return FP_ERR_INVALID_ARG;
   if (p->min_budget_blocks > FP_MAX_MIN_BUDGET) return FP_ERR_UNSUPPORTED;
-  if (p->softmax_scale < 0.f || isnan(p->softmax_scale) || isinf(p->softmax_scale))
-    return FP_ERR_INVALID_ARG;
+  if (!scale_ok(p->softmax_scale)) return FP_ERR_INVALID_ARG;
   if (p->force_pattern < -1 || p->force_pattern > 1) return FP_ERR_INVALID_ARG;
   if (p->max_budget_blocks < 0 || p->max_budget_blocks == 1) return FP_ERR_INVALID_ARG;
   if (p->max_budget_blocks > 0 && p->max_budget_blocks < p->min_budget_blocks)
@@ -194,7 +199,7 @@ fp_status fp_validate(const fp_shape *shape, const fp_params *params, size_t ws_
 }
 
 fp_status fp_select(const fp_shape *shape, const void *q, const void *k, const fp_params *params,
-                    const fp_indices *out, void *ws, size_t ws_bytes, void *stream) {
+                    fp_indices *out, void *ws, size_t ws_bytes, void *stream) {
   fp_status st = fp_validate(shape, params, ws_bytes);
   if (st != FP_OK) return st;
   if (!q || !k || !out || !out->kb_idx || !out->kb_cnt || !out->pattern || !out->js ||
@@ -214,8 +219,7 @@ fp_status fp_select(const fp_shape *shape, const void *q, const void *k, const f
   a.total_tokens = (int32_t)dm.total_tokens;
   a.nb_total = (int32_t)dm.nb_total;
   a.tri_total = dm.tri_total;
-  a.scale = params->softmax_scale > 0.f ? params->softmax_scale
-                                        : 1.0f / sqrtf((float)shape->head_dim);
+  a.scale = resolved_scale(params->softmax_scale, shape->head_dim);
   a.gamma = params->gamma;
   a.tau = params->tau;
   a.min_budget = params->min_budget_blocks;
@@ -228,6 +232,7 @@ fp_status fp_select(const fp_shape *shape, const void *q, const void *k, const f
   a.pattern = out->pattern;
   a.js = out->js;
   a.units = out->units;
+  out->softmax_scale = a.scale;
   hipStream_t s = (hipStream_t)stream;
   hipError_t e;
   if (params->gamma >= 1.f) {
@@ -241,14 +246,13 @@ fp_status fp_select(const fp_shape *shape, const void *q, const void *k, const f
 }
 
 fp_status fp_sparse_attn(const fp_shape *shape, const void *q, const void *k, const void *v,
-                         const fp_indices *idx, float softmax_scale, void *o, void *ws,
-                         size_t ws_bytes, void *stream) {
+                         const fp_indices *idx, void *o, void *ws, size_t ws_bytes,
+                         void *stream) {
   fp_status st = fp_validate(shape, nullptr, ws_bytes);
   if (st != FP_OK) return st;
   if (!q || !k || !v || !o || !idx || !idx->kb_idx || !idx->kb_cnt || !ws)
     return FP_ERR_INVALID_ARG;
-  if (softmax_scale < 0.f || isnan(softmax_scale) || isinf(softmax_scale))
-    return FP_ERR_INVALID_ARG;
+  if (!scale_ok(idx->softmax_scale)) return FP_ERR_INVALID_ARG;
   Dims dm;
   check_shape(shape, &dm);
   fp::AttnArgs a;
@@ -266,9 +270,7 @@ fp_status fp_sparse_attn(const fp_shape *shape, const void *q, const void *k, co
   a.block = shape->block;
   a.nb_total = (int32_t)dm.nb_total;
   a.tri_total = dm.tri_total;
-  const float scale =
-      softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)shape->head_dim);
-  a.scale_log2 = scale * 1.4426950408889634f;
+  a.scale_log2 = resolved_scale(idx->softmax_scale, shape->head_dim) * 1.4426950408889634f;
   a.items = (int4 *)ws;
   a.queue = (int32_t *)((char *)ws + align_up(16 * dm.nb_total * shape->num_q_heads));
   a.vt = (uint16_t *)((char *)a.queue + align_up(8 * sizeof(int32_t)));

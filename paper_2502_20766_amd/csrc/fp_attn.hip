@@ -526,7 +526,6 @@ void sparse_fa_fwd(AttnArgs a) {
     const int n_stages = max(2 * cur.cnt, 1);
     for (int t = 0; t < n_stages; ++t) {
       const int k0 = k0_next;
-      const uint8_t *ks = lds + buf * 2 * S::BYTES;
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's DMA of stage t landed
       barrier();                        // ... and every wave's; stage t-1 reads are done
       fetch_step();

@@ -130,12 +130,12 @@ def test_null_pointers_rejected_before_any_launch(lib):
     assert lib.fp_validate(None, ctypes.byref(p), 0) == fpx.FP_ERR_INVALID_ARG
     bad = fpx.FpShape(1, None, 2, 2, 64, 128)
     assert lib.fp_validate(ctypes.byref(bad), ctypes.byref(p), 1 << 40) == fpx.FP_ERR_INVALID_ARG
-    idx = fpx.FpIndices(None, None, None, None, None)
+    idx = fpx.FpIndices(None, None, None, None, None, 0.0)
     # null tensors: rejected on the host, nothing enqueued
     st = lib.fp_select(ctypes.byref(sh.c), None, None, ctypes.byref(p), ctypes.byref(idx), None,
                        1 << 30, None)
     assert st == fpx.FP_ERR_INVALID_ARG
-    st = lib.fp_sparse_attn(ctypes.byref(sh.c), None, None, None, ctypes.byref(idx), 0.0, None,
+    st = lib.fp_sparse_attn(ctypes.byref(sh.c), None, None, None, ctypes.byref(idx), None,
                             None, 1 << 30, None)
     assert st == fpx.FP_ERR_INVALID_ARG
     # workspace check comes first for a too-small size
@@ -152,3 +152,64 @@ def test_product_path_has_no_oracle_dependency():
             if f.endswith((".py", ".hip", ".cpp", ".h")):
                 text = open(os.path.join(root, f)).read()
                 assert "import oracle" not in text and "from oracle" not in text, f
+
+
+@pytest.mark.parametrize("scale,status", [
+    (-1.0, fpx.FP_ERR_INVALID_ARG), (float("nan"), fpx.FP_ERR_INVALID_ARG),
+    (float("inf"), fpx.FP_ERR_INVALID_ARG)])
+def test_attention_scale_comes_from_the_indices_and_is_checked(lib, scale, status):
+    """fp_sparse_attn takes its softmax scale from fp_indices.softmax_scale (the scale
+    fp_select used); an invalid one is rejected on the host before anything is enqueued.
+    The pointers are never dereferenced: the check fails first."""
+    sh = _shape()
+    ws = fpx.attn_workspace_size(sh)
+    fake = ctypes.c_void_p(16)
+    idx = fpx.FpIndices(16, 16, 16, 16, 16, scale)
+    st = lib.fp_sparse_attn(ctypes.byref(sh.c), fake, fake, fake, ctypes.byref(idx), fake, fake,
+                            ws, None)
+    assert st == status
+
+
+def test_fp_indices_layout_matches_the_header():
+    """The binding's ctypes mirror of fp_indices has the header's field order and offsets."""
+    text = open(HEADER).read()
+    body = re.search(r"typedef struct fp_indices \{(.*?)\} fp_indices;", text, re.S).group(1)
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    fields = re.findall(r"\b([a-z_]+);", body)
+    assert fields == [f[0] for f in fpx.FpIndices._fields_]
+    assert fpx.FpIndices.softmax_scale.offset == 5 * ctypes.sizeof(ctypes.c_void_p)
+
+
+SH = dict(cu=(0, 300, 1000), hq=4, hkv=2, d=128)
+
+
+@pytest.mark.parametrize("kw,ok", [
+    (dict(q=(1000, 4, 128), k=(1000, 2, 128), v=(1000, 2, 128), o=(1000, 4, 128)), True),
+    (dict(q=(999, 4, 128)), False),                 # T differs from cu_seqlens[-1]
+    (dict(k=(1001, 2, 128)), False),
+    (dict(q=(1000, 2, 128)), False),                # query heads
+    (dict(k=(1000, 4, 128)), False),                # KV heads
+    (dict(k=(1000, 2, 64)), False),                 # head dim
+    (dict(v=(1000, 2, 64)), False),                 # v must match k
+    (dict(o=(1000, 4, 64)), False),                 # out must match q
+    (dict(o=(1000, 4)), False),
+])
+def test_check_shapes_tensors(lib, kw, ok):
+    sh = _shape(**SH)
+    if ok:
+        fpx.check_shapes(sh, **kw)
+    else:
+        with pytest.raises(ValueError):
+            fpx.check_shapes(sh, **kw)
+
+
+def test_check_shapes_index_buffers(lib):
+    sh = _shape(**SH)
+    n_idx, n_cnt = fpx.indices_size(sh)
+    b, hq = 2, 4
+    fpx.check_shapes(sh, index_lens=(n_idx, n_cnt, b * hq, b * hq, b * hq * 2))
+    for i, short in enumerate((n_idx - 1, n_cnt - 1, b * hq - 1, b * hq - 1, b * hq * 2 - 1)):
+        lens = [n_idx, n_cnt, b * hq, b * hq, b * hq * 2]
+        lens[i] = short
+        with pytest.raises(ValueError):
+            fpx.check_shapes(sh, index_lens=tuple(lens))

@@ -31,11 +31,12 @@ def _fpx():
 
 
 def run_gpu(layer, gamma, tau, min_budget, force_pattern=-1, max_budget=0, qa_mode=0,
-            vs_granularity=0):
+            vs_granularity=0, softmax_scale=0.0):
     fpx = _fpx()
     q, k, v = to_device(layer)
     idx = fpx.select(q, k, layer.cu_seqlens, gamma, tau, min_budget, force_pattern=force_pattern,
-                     max_budget=max_budget, qa_mode=qa_mode, vs_granularity=vs_granularity)
+                     max_budget=max_budget, qa_mode=qa_mode, vs_granularity=vs_granularity,
+                     softmax_scale=softmax_scale)
     o = fpx.sparse_attn(q, k, v, idx)
     torch.cuda.synchronize()
     return dict(masks=fpx.masks_from_indices(idx), pattern=idx.pattern.cpu().numpy(),
@@ -156,6 +157,26 @@ def test_select_and_attention_vs_oracle(case):
     log(f"  {st}")
     assert_relaxations_bounded(st)
     mx, mean = compare_outputs(layer, g["o"], g["masks"], rows_per_head=6)
+    log(f"  output max_abs {mx:.3e} mean_abs {mean:.3e}")
+    assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
+
+
+@pytest.mark.parametrize("scale_factor", [0.6, 1.5])
+def test_non_default_softmax_scale(scale_factor):
+    """A softmax scale other than 1/sqrt(d): the selection (every kernel that scales
+    logits) and the attention (which takes the scale fp_select recorded in the indices)
+    against the oracle run with the same scale."""
+    spec = SELECT_CASES[1][1]
+    scale = scale_factor / math.sqrt(spec.d)
+    log(f"[softmax scale {scale:.5f}] {spec.name}")
+    layer = synth.make_layer(spec)
+    g = run_gpu(layer, spec.gamma, spec.tau, spec.min_budget, softmax_scale=scale)
+    assert abs(g["idx"].softmax_scale - scale) <= 1e-7 * scale
+    with Timer("oracle selection"):
+        st = compare_selection(layer, g, spec.gamma, spec.tau, spec.min_budget, scale=scale)
+    log(f"  {st}")
+    assert_relaxations_bounded(st)
+    mx, mean = compare_outputs(layer, g["o"], g["masks"], rows_per_head=6, scale=scale)
     log(f"  output max_abs {mx:.3e} mean_abs {mean:.3e}")
     assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
 
