@@ -144,6 +144,21 @@ fp_status fp_sparse_attn(const fp_shape *shape, const void *q, const void *k,
                          const void *v, const fp_indices *idx, void *o, void *ws,
                          size_t ws_bytes, void *stream);
 
+/* Size of the fixed device scratch array used by fp_sparse_attn_noalloc (one per GPU). */
+#define FP_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* fp_sparse_attn without a workspace argument, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, result and checks as fp_sparse_attn; the workspace is a
+ * fixed FP_NOALLOC_SCRATCH_BYTES device array inside the library (one per GPU, held until
+ * the process ends), so the call itself allocates nothing.  Problems whose
+ * fp_attn_workspace_size exceeds FP_NOALLOC_SCRATCH_BYTES are rejected with
+ * FP_ERR_WORKSPACE before anything is enqueued (fp_last_error() says why).  Every call on
+ * one GPU uses the same array: calls that overlap in time on one GPU (other streams, other
+ * host threads) race and give undefined results. */
+fp_status fp_sparse_attn_noalloc(const fp_shape *shape, const void *q, const void *k,
+                                 const void *v, const fp_indices *idx, void *o, void *stream);
+
 /* Static description of a status code. */
 const char *fp_status_string(fp_status status);
 

@@ -69,12 +69,13 @@ def lib() -> ctypes.CDLL:
         h.fp_validate.argtypes = [S, P, ctypes.c_size_t]
         h.fp_select.argtypes = [S, vp, vp, P, X, vp, ctypes.c_size_t, vp]
         h.fp_sparse_attn.argtypes = [S, vp, vp, vp, X, vp, vp, ctypes.c_size_t, vp]
+        h.fp_sparse_attn_noalloc.argtypes = [S, vp, vp, vp, X, vp, vp]
         h.fp_status_string.argtypes = [ctypes.c_int]
         h.fp_status_string.restype = ctypes.c_char_p
         h.fp_last_error.argtypes = []
         h.fp_last_error.restype = ctypes.c_char_p
         for name in ("fp_indices_size", "fp_select_workspace_size", "fp_attn_workspace_size",
-                     "fp_validate", "fp_select", "fp_sparse_attn"):
+                     "fp_validate", "fp_select", "fp_sparse_attn", "fp_sparse_attn_noalloc"):
             getattr(h, name).restype = ctypes.c_int
         _lib_handle = h
     return _lib_handle
@@ -264,6 +265,27 @@ def sparse_attn(q, k, v, indices: Indices, out=None, workspace=None, stream=None
                                 ctypes.byref(ic), ctypes.c_void_p(out.data_ptr()),
                                 ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
                                 _stream_ptr(stream)), "fp_sparse_attn")
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20     # FP_NOALLOC_SCRATCH_BYTES
+
+
+def sparse_attn_noalloc(q, k, v, indices: Indices, out, stream=None):
+    """sparse_attn through fp_sparse_attn_noalloc: no workspace argument, the library's fixed
+    device scratch array instead (problems up to NOALLOC_SCRATCH_BYTES of workspace).
+    `out` is required: this call allocates nothing."""
+    for name, x in (("q", q), ("k", k), ("v", v), ("out", out)):
+        _check_tensor(x, name, 3)
+    shape = indices.shape
+    check_shapes(shape, q=q.shape, k=k.shape, v=v.shape, o=out.shape)
+    _check_indices(indices, shape)
+    ic = indices.c()
+    _check(lib().fp_sparse_attn_noalloc(ctypes.byref(shape.c), ctypes.c_void_p(q.data_ptr()),
+                                        ctypes.c_void_p(k.data_ptr()),
+                                        ctypes.c_void_p(v.data_ptr()), ctypes.byref(ic),
+                                        ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)),
+           "fp_sparse_attn_noalloc")
     return out
 
 

@@ -14,7 +14,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libflexprefill.so")
 OBJ_DIR = os.path.join(PKG, "_build")
-SOURCES = ["fp_attn.hip", "fp_scores.hip", "fp_pattern.hip", "fp_select.hip", "fp_api.cpp"]
+SOURCES = ["fp_attn.hip", "fp_scores.hip", "fp_pattern.hip", "fp_select.hip", "fp_noalloc.hip",
+           "fp_api.cpp"]
 ARCH = "gfx950"
 # Packed fp32 instructions are disabled for every device compilation.
 # Warnings are errors on both the host and the device pass.

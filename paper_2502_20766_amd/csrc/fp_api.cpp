@@ -278,6 +278,27 @@ fp_status fp_sparse_attn(const fp_shape *shape, const void *q, const void *k, co
   return e == hipSuccess ? FP_OK : hip_fail(e, "fp_sparse_attn");
 }
 
+fp_status fp_sparse_attn_noalloc(const fp_shape *shape, const void *q, const void *k,
+                                 const void *v, const fp_indices *idx, void *o, void *stream) {
+  Dims dm;
+  fp_status st = check_shape(shape, &dm);
+  if (st != FP_OK) return st;
+  const size_t need = attn_layout(shape, dm);
+  if (need > (size_t)FP_NOALLOC_SCRATCH_BYTES) {
+    snprintf(g_last_error, sizeof(g_last_error),
+             "fp_sparse_attn_noalloc: the problem needs %zu workspace bytes, more than the "
+             "fixed scratch of %zu",
+             need, (size_t)FP_NOALLOC_SCRATCH_BYTES);
+    return FP_ERR_WORKSPACE;
+  }
+  if (!q || !k || !v || !o || !idx || !idx->kb_idx || !idx->kb_cnt) return FP_ERR_INVALID_ARG;
+  if (!scale_ok(idx->softmax_scale)) return FP_ERR_INVALID_ARG;
+  void *ws = nullptr;
+  const hipError_t e = fp::noalloc_scratch(&ws);
+  if (e != hipSuccess) return hip_fail(e, "fp_sparse_attn_noalloc(scratch)");
+  return fp_sparse_attn(shape, q, k, v, idx, o, ws, (size_t)FP_NOALLOC_SCRATCH_BYTES, stream);
+}
+
 const char *fp_status_string(fp_status status) {
   switch (status) {
     case FP_OK: return "FP_OK";

@@ -96,6 +96,9 @@ struct AttnArgs {
   uint16_t *vt;            // [Hkv][NB][B * d] workspace: V^T tiles per key block
 };
 
+// Device address of the current device's fixed scratch array (fp_noalloc.hip).
+hipError_t noalloc_scratch(void **out);
+
 // Launchers (each returns the hipError_t of its launch).
 hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t s);
 hipError_t launch_select_pipeline(const SelectArgs &a, hipStream_t s);
