@@ -78,6 +78,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-sdpa", action="store_true", help="skip the PyTorch SDPA dense timing")
+    ap.add_argument("--no-gemm", action="store_true",
+                    help="skip the bf16 GEMM ceiling measured beside the attention kernel")
     ap.add_argument("--cpu-sample-heads", type=int, default=32)
     ap.add_argument("--cpu-sample-rows", type=int, default=32)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -122,6 +124,11 @@ def sample_clocks(enqueue, seconds, per_call_ms):
     `enqueue()` calls (about `seconds` of GPU work) are running; None without amd-smi."""
     import subprocess
     import torch
+    # under a profiler the preloaded tool library would initialise the GPU in the amd-smi
+    # child too, and that child replaces itself with its interpreter: not done there
+    if any(k.startswith("ROCPROF") for k in os.environ) or "rocprof" in os.environ.get(
+            "LD_PRELOAD", ""):
+        return {"skipped": "running under a profiler"}
     n = max(2, int(math.ceil(seconds * 1e3 / max(per_call_ms, 1e-3))))
     for _ in range(n):
         enqueue()
@@ -158,6 +165,24 @@ def causal_exact_flop(idx, shape, d):
     cnt = cnt[:hq * rows.size].reshape(hq, rows.size)
     pairs = np.where(cnt > 0, (cnt - 1) * rows[None, :] * b + rows * (rows + 1) // 2, 0)
     return float(4 * d * pairs.sum())
+
+
+def gemm_ceiling(stream, n=8192, steps=30):
+    """Sustained rate of the platform's bf16 GEMM (torch.matmul -> hipBLASLt) on n x n x n,
+    with the clocks read while it runs: the MFMA rate this GPU holds under its power limit
+    for a plain dense contraction, measured beside the attention kernel."""
+    import torch
+    a = torch.randn(n, n, device="cuda:0").to(torch.bfloat16)
+    b = torch.randn(n, n, device="cuda:0").to(torch.bfloat16)
+    c = torch.empty(n, n, device="cuda:0", dtype=torch.bfloat16)
+    for _ in range(5):
+        torch.matmul(a, b, out=c)
+    ms = time_loop(lambda: torch.matmul(a, b, out=c), steps, stream)
+    tflops = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+    clocks = sample_clocks(lambda: torch.matmul(a, b, out=c), 1.5, ms)
+    del a, b, c
+    return {"shape": [n, n, n], "ms": round(ms, 4), "tflops": round(tflops, 1),
+            "frac_of_peak": round(tflops / PEAK_BF16_TFLOPS, 4), "clocks": clocks}
 
 
 def time_loop(fn, steps, stream):
@@ -417,6 +442,11 @@ def main():
     f_exact = causal_exact_flop(idx, shape, spec.d)
     log("[bench] clocks under the attention kernel")
     clocks = sample_clocks(do_attn, 1.5, ms_attn)
+    gemm = None
+    if not args.no_gemm:
+        log("[bench] bf16 GEMM ceiling (torch.matmul 8192^3)")
+        gemm = gemm_ceiling(stream)
+        log(f"[bench] GEMM {gemm['tflops']} TFLOP/s")
 
     gamma_table = None
     gammas = ([float(x) for x in args.gammas.split(",")] if args.gammas
@@ -489,6 +519,7 @@ def main():
                               "kernel), hipEvents on the launch stream"},
         "attn_tflops_causal_exact": round(f_exact / (ms_attn * 1e-3) / 1e12, 2),
         "clocks_under_attention": clocks,
+        "bf16_gemm_ceiling": gemm,
         "run": run_metadata(),
     }
     if gamma_table is not None:
