@@ -78,6 +78,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-sdpa", action="store_true", help="skip the PyTorch SDPA dense timing")
+    ap.add_argument("--probe", action="store_true",
+                    help="run the stage-mix probe (built by __graft_entry__.build()) instead of "
+                         "the benchmark and print its JSON")
     ap.add_argument("--no-gemm", action="store_true",
                     help="skip the bf16 GEMM ceiling measured beside the attention kernel")
     ap.add_argument("--cpu-sample-heads", type=int, default=32)
@@ -183,6 +186,21 @@ def gemm_ceiling(stream, n=8192, steps=30):
     del a, b, c
     return {"shape": [n, n, n], "ms": round(ms, 4), "tflops": round(tflops, 1),
             "frac_of_peak": round(tflops / PEAK_BF16_TFLOPS, 4), "clocks": clocks}
+
+
+def probe():
+    """The attention stage's instruction mix without the kernel's row logic, in four modes
+    (alone, + barrier, + K/V copies, MFMA and fragment reads only): see bench_probe.hip."""
+    import subprocess
+    exe = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_build", "bench_probe")
+    if not os.path.exists(exe):
+        raise SystemExit(f"{exe} is missing: run __graft_entry__.build() first")
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=300)
+    if r.returncode != 0:
+        raise SystemExit(f"bench_probe failed ({r.returncode}): {r.stderr[-2000:]}")
+    out = json.loads(r.stdout)
+    out["peak_tflops"] = PEAK_BF16_TFLOPS
+    print(json.dumps(out), flush=True)
 
 
 def time_loop(fn, steps, stream):
@@ -332,6 +350,9 @@ def main():
         sys.exit(2)
     if args.sweep:
         sweep(args)
+        return
+    if args.probe:
+        probe()
         return
     import torch
     import synth
