@@ -124,7 +124,9 @@ def run_metadata():
 
 def sample_clocks(enqueue, seconds, per_call_ms):
     """Shader clocks (MHz, one per XCD) and socket power (W) read with amd-smi while
-    `enqueue()` calls (about `seconds` of GPU work) are running; None without amd-smi."""
+    `enqueue()` calls (about `seconds` of GPU work) are running; None without amd-smi.
+    `gpu_busy_when_read` is false when the queued work had already drained by the time the
+    reading returned (the figures then describe an idle or ramping GPU)."""
     import subprocess
     import torch
     # under a profiler the preloaded tool library would initialise the GPU in the amd-smi
@@ -135,11 +137,14 @@ def sample_clocks(enqueue, seconds, per_call_ms):
     n = max(2, int(math.ceil(seconds * 1e3 / max(per_call_ms, 1e-3))))
     for _ in range(n):
         enqueue()
+    done = torch.cuda.Event()
+    done.record()
     out = None
     try:
-        time.sleep(0.2)
+        time.sleep(1.0)                 # past the clock ramp, well before the queue drains
         r = subprocess.run(["amd-smi", "metric", "-c", "-p", "--json"], capture_output=True,
                            text=True, timeout=30)
+        busy = not done.query()
         if r.returncode == 0:
             data = json.loads(r.stdout)
             g = data["gpu_data"][0] if isinstance(data, dict) else data[0]
@@ -149,7 +154,7 @@ def sample_clocks(enqueue, seconds, per_call_ms):
                    and isinstance(v.get("clk"), dict) and str(v["clk"].get("value")).isdigit()]
             pw = g.get("power", {}).get("socket_power", {}).get("value")
             out = {"gfx_mhz": gfx, "gfx_mhz_mean": round(sum(gfx) / len(gfx), 1) if gfx else None,
-                   "socket_power_w": pw, "calls_in_flight": n}
+                   "socket_power_w": pw, "calls_queued": n, "gpu_busy_when_read": busy}
     except Exception as e:  # noqa: BLE001
         out = {"error": str(e)[:200]}
     torch.cuda.synchronize()
@@ -182,7 +187,7 @@ def gemm_ceiling(stream, n=8192, steps=30):
         torch.matmul(a, b, out=c)
     ms = time_loop(lambda: torch.matmul(a, b, out=c), steps, stream)
     tflops = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
-    clocks = sample_clocks(lambda: torch.matmul(a, b, out=c), 1.5, ms)
+    clocks = sample_clocks(lambda: torch.matmul(a, b, out=c), 5.0, ms)
     del a, b, c
     return {"shape": [n, n, n], "ms": round(ms, 4), "tflops": round(tflops, 1),
             "frac_of_peak": round(tflops / PEAK_BF16_TFLOPS, 4), "clocks": clocks}
@@ -462,7 +467,7 @@ def main():
     dense_ms = min([x for kk, x in dense.items() if kk.endswith("_ms")] or [float("nan")])
     f_exact = causal_exact_flop(idx, shape, spec.d)
     log("[bench] clocks under the attention kernel")
-    clocks = sample_clocks(do_attn, 1.5, ms_attn)
+    clocks = sample_clocks(do_attn, 5.0, ms_attn)
     gemm = None
     if not args.no_gemm:
         log("[bench] bf16 GEMM ceiling (torch.matmul 8192^3)")

@@ -4,7 +4,7 @@
 // LDS reads and 16 MFMAs (S^T = K Q^T over 64 keys x 32 queries x d 128), the row max, 32
 // exponentials with their scale FMAs, bf16 packing and row sums, then 16 V^T-fragment LDS
 // reads and 16 MFMAs (O^T += V^T P^T) -- on a persistent grid of two 4-wave workgroups per
-// CU (the kernel's occupancy), with none of the kernel's row logic, in six modes:
+// CU (the kernel's occupancy), with none of the kernel's row logic, in seven modes:
 //   mode 0  the mix alone (one LDS tile pair, no barrier, no copies);
 //   mode 1  plus one workgroup barrier per stage;
 //   mode 2  plus the stage copies: K and V^T tiles (16 KB each) copied global -> LDS with
@@ -13,7 +13,8 @@
 //   mode 3  the MFMAs and fragment reads only (no softmax work), no barrier, no copies;
 //   mode 4  mode 0 with the P V product one stage behind: the previous stage's 16 PV MFMAs
 //           issued one by one between this stage's exponentials (scheduling fences);
-//   mode 5  mode 0 with the wave priority raised around its MFMA groups (s_setprio).
+//   mode 5  mode 0 with the wave priority raised around its MFMA groups (s_setprio);
+//   mode 6  the mix as a ping-pong of two 4-wave groups in one 8-wave workgroup per CU.
 // Each mode reports the MFMA rate over its launches (hipEvents); the clock and the
 // matrix-pipe busy fraction come from a counter pass over the same program (GRBM_GUI_ACTIVE,
 // SQ_VALU_MFMA_BUSY_CYCLES).  Operands are hashed finite bf16 values
@@ -215,6 +216,96 @@ __global__ __launch_bounds__(kThreads) void stage_mix(int stages, const uint4 *s
   sink[(size_t)blockIdx.x * kThreads + tid] = s;
 }
 
+// mode 6: one 8-wave workgroup per CU (the same two waves per SIMD); waves 0-3 and 4-7
+// alternate an MFMA phase (the previous stage's P V, then this stage's Q K) and a VALU phase
+// (the softmax of that stage), switched at workgroup barriers, so that the two waves of a
+// SIMD are always in opposite phases.  LDS: one K tile and one V^T tile (32 KB).
+__global__ __launch_bounds__(2 * kThreads) void ping_pong(int stages, float *sink) {
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * kTile];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, grp = w >> 2;
+  for (int i = tid; i < 2 * kTile / 4; i += 2 * kThreads)
+    reinterpret_cast<uint32_t *>(lds)[i] = hashed_bf16x2(0x40000u + (uint32_t)i);
+  __syncthreads();
+  bf16x8 qf[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    uint32_t u[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      u[e] = hashed_bf16x2(0x80000u + 64u * (32u * k + 4u * e) + lane + 4096u * w);
+    qf[k] = __builtin_bit_cast(bf16x8, make_uint4(u[0], u[1], u[2], u[3]));
+  }
+  f32x16 oacc[4] = {};
+  f32x16 sacc[2] = {};
+  bf16x8 pf[4] = {};
+  float l_run = 0.f, m_ref = 0.f;
+  const float c = 0.12751743f;
+  const uint32_t lane_off = 16u * (uint32_t)lane;
+  const uint8_t *kt = lds, *vt = lds + kTile;
+  auto mfma_phase = [&](int t) {
+    const uint32_t rot = 16u * (uint32_t)(t & 3);
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      bf16x8 vf[4];
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+        vf[db] = *reinterpret_cast<const bf16x8 *>(vt + ((lane_off ^ rot) + db * 1024 + st * 4096));
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db], pf[st], oacc[db], 0, 0, 0);
+    }
+#pragma unroll
+    for (int b2 = 0; b2 < 2; ++b2) {
+      sacc[b2] = f32x16{};
+      bf16x8 kf[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        kf[k] = *reinterpret_cast<const bf16x8 *>(kt + ((lane_off ^ rot) + k * 1024 + b2 * 8192));
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[k], qf[k], sacc[b2], 0, 0, 0);
+    }
+  };
+  auto valu_phase = [&]() {
+    float mt = m_ref;
+#pragma unroll
+    for (int b2 = 0; b2 < 2; ++b2)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sacc[b2][v]);
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(mt), __float_as_uint(mt), false,
+                                              false);
+    m_ref = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    const float mc = m_ref * c;
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int v = 0; v < 8; ++v)
+        pf[st][v] = (__bf16)__builtin_amdgcn_exp2f(fmaf(sacc[st >> 1][8 * (st & 1) + v], c, -mc));
+    const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bf16x2 pair = {pf[st][2 * e], pf[st][2 * e + 1]};
+        l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, one, l_run, false);
+      }
+  };
+  for (int t = 0; t < stages; ++t) {
+    if (grp == 0) mfma_phase(t);
+    else valu_phase();
+    __builtin_amdgcn_s_barrier();
+    if (grp == 0) valu_phase();
+    else mfma_phase(t);
+    __builtin_amdgcn_s_barrier();
+  }
+  float s = l_run + m_ref;
+#pragma unroll
+  for (int db = 0; db < 4; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s += oacc[db][i];
+  sink[(size_t)blockIdx.x * 2 * kThreads + tid] = s;
+}
+
 bool check(hipError_t e, const char *what) {
   if (e != hipSuccess) {
     fprintf(stderr, "%s: %s\n", what, hipGetErrorString(e));
@@ -245,6 +336,26 @@ bool run_mode(int nblk, int stages, const uint4 *src, float *d_sink,
   return check(hipEventDestroy(e0), "event") && check(hipEventDestroy(e1), "event");
 }
 
+bool run_ping_pong(int cus, int stages, float *d_sink) {
+  hipEvent_t e0, e1;
+  if (!check(hipEventCreate(&e0), "event") || !check(hipEventCreate(&e1), "event")) return false;
+  hipLaunchKernelGGL(ping_pong, dim3(cus), dim3(2 * kThreads), 0, 0, 16, d_sink);
+  if (!check(hipDeviceSynchronize(), "warm-up launch")) return false;
+  constexpr int kReps = 3;
+  if (!check(hipEventRecord(e0, 0), "event")) return false;
+  for (int r = 0; r < kReps; ++r)
+    hipLaunchKernelGGL(ping_pong, dim3(cus), dim3(2 * kThreads), 0, 0, stages, d_sink);
+  if (!check(hipEventRecord(e1, 0), "event")) return false;
+  if (!check(hipEventSynchronize(e1), "timed launches")) return false;
+  float ms = 0.f;
+  if (!check(hipEventElapsedTime(&ms, e0, e1), "event")) return false;
+  ms /= kReps;
+  const double flop = (double)cus * 8 * 32 * 32768.0 * stages;
+  printf("    {\"mode\": 6, \"what\": \"ping-pong of two 4-wave groups\", \"ms\": %.3f, "
+         "\"tflops\": %.1f}\n", ms, flop / (ms * 1e-3) / 1e12);
+  return check(hipEventDestroy(e0), "event") && check(hipEventDestroy(e1), "event");
+}
+
 }  // namespace
 
 int main(int argc, char **argv) {
@@ -272,7 +383,8 @@ int main(int argc, char **argv) {
                         false) &&
             run_mode<3>(nblk, stages, src, d_sink, "MFMAs and fragment reads only", false) &&
             run_mode<4>(nblk, stages, src, d_sink, "PV of previous stage between exps", false) &&
-            run_mode<5>(nblk, stages, src, d_sink, "mix with setprio around MFMAs", true);
+            run_mode<5>(nblk, stages, src, d_sink, "mix with setprio around MFMAs", false) &&
+            run_ping_pong(cus, stages, d_sink);
   printf("]}\n");
   ok = check(hipFree(src), "free") && check(hipFree(d_sink), "free") && ok;
   return ok ? 0 : 1;
