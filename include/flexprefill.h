@@ -17,6 +17,10 @@
  *  - Query head h reads KV head h / (Hq / Hkv) (grouped-query attention).
  *  - Every device pointer is caller-owned device memory; the library never
  *    allocates, frees, or synchronises, and never throws across the ABI.
+ *  - The compute calls enqueue kernel launches only (no memset or copy nodes, no host
+ *    waits), so they can be captured into a HIP graph and replayed; the first call of
+ *    fp_sparse_attn_noalloc on a device resolves its scratch address and belongs
+ *    outside a capture.
  *  - All arguments are checked on the host before anything is enqueued; on a
  *    failed check the first failing status is returned and nothing is enqueued.
  *  - Work is enqueued on `stream` (a hipStream_t; NULL = the default stream) and
