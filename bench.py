@@ -209,14 +209,25 @@ def probe():
 
 
 def time_loop(fn, steps, stream):
+    """Mean device time per call of `steps` back-to-back calls (hipEvents on `stream`).
+    Python's cyclic garbage collector is paused meanwhile: at short lengths the device work
+    of a call is comparable to its host-side enqueue, so a collection pause inside the
+    loop would leave the GPU idle and count as device time."""
+    import gc
     import torch
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     torch.cuda.synchronize()
-    ev[0].record(stream)
-    for _ in range(steps):
-        fn()
-    ev[1].record(stream)
-    torch.cuda.synchronize()
+    gc_was_enabled = gc.isenabled()
+    gc.disable()
+    try:
+        ev[0].record(stream)
+        for _ in range(steps):
+            fn()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+    finally:
+        if gc_was_enabled:
+            gc.enable()
     return ev[0].elapsed_time(ev[1]) / steps
 
 

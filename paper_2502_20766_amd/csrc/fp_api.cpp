@@ -38,6 +38,18 @@ fp_status check_shape(const fp_shape *sh, Dims *dm) {
   memset(dm, 0, sizeof(*dm));
   fp::SeqTable &st = dm->st;
   st.n_seq = sh->batch;
+  // score chunk: the longest of 1024, 512, 256 keys that still gives the line-sum kernel
+  // kScoreWorkgroups (sequence chunk, query head) workgroups
+  st.ch_len = fp::kScoreChunkMin;
+  for (int len = fp::kScoreChunk; len > fp::kScoreChunkMin; len /= 2) {
+    int64_t chunks = 0;
+    for (int s = 0; s < sh->batch; ++s)
+      chunks += ((int64_t)sh->cu_seqlens[s + 1] - sh->cu_seqlens[s] + len - 1) / len;
+    if (chunks * sh->num_q_heads >= fp::kScoreWorkgroups) {
+      st.ch_len = len;
+      break;
+    }
+  }
   int64_t nb_acc = 0, tri_acc = 0, ch_acc = 0;
   int max_nb = 0;
   for (int s = 0; s < sh->batch; ++s) {
@@ -51,7 +63,7 @@ fp_status check_shape(const fp_shape *sh, Dims *dm) {
     st.ch_off[s] = (int32_t)ch_acc;
     nb_acc += nb;
     tri_acc += nb * (nb + 1) / 2;
-    ch_acc += (n + fp::kScoreChunk - 1) / fp::kScoreChunk;
+    ch_acc += (n + st.ch_len - 1) / st.ch_len;
     if (nb > max_nb) max_nb = (int)nb;
   }
   const int64_t T = sh->cu_seqlens[sh->batch];

@@ -213,6 +213,7 @@ struct Row {
 };
 
 constexpr int kChunk = 16;   // consecutive ordered items kept together on one XCD
+constexpr int kMixItems = 8;    // at most this many items per workgroup: groups interleaved
 
 // Item v of XCD x's work queue -> (KV group g, index j into g's ordered items), false once
 // the queue is exhausted (every later v is then exhausted too).
@@ -224,14 +225,28 @@ constexpr int kChunk = 16;   // consecutive ordered items kept together on one X
 //    chunks of kChunk, dealt round-robin, so similar items stay on one XCD's L2;
 //  * otherwise XCD x takes the whole lists of groups x, x + 8, ... in turn (XCDs without a
 //    group only steal).
-__device__ __forceinline__ bool queue_item(int x, int v, int hkv, int n_g, int &g, int &j) {
+// With `mix` (short problems: few items per workgroup) an XCD that serves several groups
+// takes their items alternately, one from each, instead of one group after the other: each
+// group's items are ordered longest first, so the longest items of every group start in
+// the first round instead of the later groups' after the earlier groups' short ones.
+__device__ __forceinline__ bool queue_item(int x, int v, int hkv, int n_g, int mix, int &g,
+                                           int &j) {
   if (hkv % 4 == 0 && hkv >= 8) {
     const int half = x >> 2;                        // which XCD of the pair
     const int nch = (n_g + kChunk - 1) / kChunk;    // chunks per group
     int taken = ((nch - half + 1) / 2) * kChunk;    // items of one group this XCD takes
     if (((nch - 1) & 1) == half) taken -= nch * kChunk - n_g;   // it holds the short chunk
     if (taken <= 0) return false;
-    const int q = v / taken, vv = v % taken;
+    int q, vv;
+    if (mix) {                                      // the XCD's groups item by item
+      const int ng = hkv / 4;
+      if (v >= ng * taken) return false;
+      q = v % ng;
+      vv = v / ng;
+    } else {                                        // one group after the other
+      q = v / taken;
+      vv = v % taken;
+    }
     g = (x & 3) + 4 * q;
     j = ((vv / kChunk) * 2 + half) * kChunk + vv % kChunk;
     return g < hkv && j < n_g;
@@ -241,6 +256,13 @@ __device__ __forceinline__ bool queue_item(int x, int v, int hkv, int n_g, int &
     g = x % hkv;
     j = ((v / kChunk) * r + x / hkv) * kChunk + v % kChunk;
     return j < n_g;
+  }
+  if (mix) {                                        // the XCD's groups item by item
+    const int ng = x < hkv ? (hkv - x + 7) / 8 : 0;
+    if (v >= ng * n_g) return false;
+    g = x + 8 * (v % ng);
+    j = v / ng;
+    return true;
   }
   g = x + 8 * (v / n_g);
   j = v % n_g;
@@ -357,7 +379,7 @@ void sparse_fa_fwd(AttnArgs a) {
   cur.valid = 0;
   {
     int g, j;
-    if (queue_item(x0, blockIdx.x >> 3, a.hkv, n_g, g, j)) {
+    if (queue_item(x0, blockIdx.x >> 3, a.hkv, n_g, a.mix, g, j)) {
       const int4 rec = a.items[(int64_t)g * n_g + j];
       cur = row_from(g, __builtin_amdgcn_readfirstlane(rec.x), __builtin_amdgcn_readfirstlane(rec.y),
                      __builtin_amdgcn_readfirstlane(rec.z), __builtin_amdgcn_readfirstlane(rec.w));
@@ -412,7 +434,7 @@ void sparse_fa_fwd(AttnArgs a) {
             P8 + __builtin_amdgcn_readfirstlane(lds_read_i32(slot_addr + 4 * (n_fetch & 1)));
         ++n_fetch;
         int g, j;
-        if (queue_item(x, v, a.hkv, n_g, g, j)) {
+        if (queue_item(x, v, a.hkv, n_g, a.mix, g, j)) {
           fetch_g = g;
           if (tid < 4) {
             const __amdgpu_buffer_rsrc_t rr = uniform_rsrc(a.items + (int64_t)g * n_g + j, 16);
@@ -913,20 +935,25 @@ hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t stream) {
   auto grid = [&](int wg_per_cu) {
     return (int)std::min<int64_t>((wg_per_cu * cus / 8) * 8, (total + 7) / 8 * 8);
   };
+  // groups interleaved on an XCD when there are at most kMixItems items per workgroup
+  AttnArgs b = a;
+  b.mix = total <= (int64_t)kMixItems * grid(a.block == 128 ? Geo<128>::WG_PER_CU
+                                                             : Geo<64>::WG_PER_CU);
+  const AttnArgs &a2 = b;
   if (a.block == 128) {
     if (a.d == 128)
       hipLaunchKernelGGL((sparse_fa_fwd<128, 128>), dim3(grid(Geo<128>::WG_PER_CU)),
-                         dim3(Geo<128>::THREADS), 0, stream, a);
+                         dim3(Geo<128>::THREADS), 0, stream, a2);
     else
       hipLaunchKernelGGL((sparse_fa_fwd<64, 128>), dim3(grid(Geo<128>::WG_PER_CU)),
-                         dim3(Geo<128>::THREADS), 0, stream, a);
+                         dim3(Geo<128>::THREADS), 0, stream, a2);
   } else {
     if (a.d == 128)
       hipLaunchKernelGGL((sparse_fa_fwd<128, 64>), dim3(grid(Geo<64>::WG_PER_CU)),
-                         dim3(Geo<64>::THREADS), 0, stream, a);
+                         dim3(Geo<64>::THREADS), 0, stream, a2);
     else
       hipLaunchKernelGGL((sparse_fa_fwd<64, 64>), dim3(grid(Geo<64>::WG_PER_CU)),
-                         dim3(Geo<64>::THREADS), 0, stream, a);
+                         dim3(Geo<64>::THREADS), 0, stream, a2);
   }
   return hipGetLastError();
 }

@@ -8,9 +8,13 @@
 
 namespace fp {
 
-// Keys of one key block processed per step of the representative-score kernels, and
-// key-chunk length owned by one workgroup of those kernels.
+// Longest key chunk owned by one workgroup of the representative-score kernels.  Short
+// problems use chunks of 512 or 256 keys (SeqTable::ch_len) so that those kernels still
+// get enough workgroups to fill the GPU.
 constexpr int kScoreChunk = 1024;
+constexpr int kScoreChunkMin = 256;
+// workgroups of the line-sum kernel wanted before the chunk is shortened (4 per CU)
+constexpr int kScoreWorkgroups = 1024;
 constexpr int kHistBuckets = 2048;     // radix-select digit: 11 bits
 
 // Per-call table of packed sequences, passed by value to every kernel.
@@ -19,7 +23,8 @@ struct SeqTable {
   int32_t max_nb;
   int32_t cu[FP_MAX_BATCH + 1];       // token offsets
   int32_t nb_off[FP_MAX_BATCH + 1];   // prefix sums of nb_s = ceil(n_s / block)
-  int32_t ch_off[FP_MAX_BATCH + 1];   // prefix sums of ceil(n_s / kScoreChunk)
+  int32_t ch_len;                     // keys per score chunk: 1024, 512 or 256
+  int32_t ch_off[FP_MAX_BATCH + 1];   // prefix sums of ceil(n_s / ch_len)
   int64_t tri_off[FP_MAX_BATCH + 1];  // prefix sums of nb_s (nb_s + 1) / 2
 };
 
@@ -93,6 +98,7 @@ struct AttnArgs {
   float scale_log2;        // softmax scale * log2(e)
   int4 *items;             // [Hkv][G * NB] workspace: ordered item records per KV group
   int32_t *queue;          // [8] workspace: per-XCD work-queue counters
+  int32_t mix;             // set by the launcher: an XCD's KV groups served interleaved
   uint16_t *vt;            // [Hkv][NB][B * d] workspace: V^T tiles per key block
 };
 

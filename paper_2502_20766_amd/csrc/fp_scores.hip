@@ -6,12 +6,12 @@
 //   a_v[j] = sum_r A_hat[r, j] / b'            (vertical lines, Algorithm 3)
 //   a_s[o] = sum_r A_hat[r, i_r - o] / b'      (slash lines, offset o = i - j)
 // A_hat is never stored: pass 1 computes each row's max and sum of exp per chunk of
-// 1024 keys, a combine kernel merges the chunks, pass 2 recomputes the scores tile by
-// tile, sums the columns in registers (one key per lane) and the diagonals through an LDS
-// tile.  Every sum is in a fixed order (no float atomics), so results are
-// bit-reproducible.  Each pass-2 workgroup owns the slash
-// offsets whose last-row key falls in its chunk and recomputes the 128 keys before the
-// chunk so that it sees those diagonals whole.
+// 1024 keys (512 or 256 for short problems, so that the passes still fill the GPU), a
+// combine kernel merges the chunks, pass 2 recomputes the scores tile by tile, sums the
+// columns in registers (one key per lane) and the diagonals through an LDS tile.  Every
+// sum is in a fixed order (no float atomics), so results are bit-reproducible for a given
+// shape.  Each pass-2 workgroup owns the slash offsets whose last-row key falls in its
+// chunk and recomputes the 128 keys before the chunk so that it sees those diagonals whole.
 //
 // Block pooling (avgpool with window block_size, aligned at token 0 of each sequence) is
 // a separate streaming kernel used for K (all KV heads) and Q (query-aware heads only).
@@ -132,8 +132,8 @@ __global__ __launch_bounds__(kThreads * HG) void rep_stats(SelectArgs a) {
   const int tok0 = a.st.cu[s];
   const int n = a.st.cu[s + 1] - tok0;
   const int bp = min(a.block, n);
-  const int c0 = (c - a.st.ch_off[s]) * kScoreChunk;
-  const int c1 = min(c0 + kScoreChunk, n);
+  const int c0 = (c - a.st.ch_off[s]) * a.st.ch_len;
+  const int c1 = min(c0 + a.st.ch_len, n);
   const int tid = threadIdx.x, w = (tid >> 6) & 3, lane = tid & 63, lr = lane & 31, lh = lane >> 5;
   const int r = 32 * w + lr;                 // representative row of this lane
   const int irow = n - bp + r;               // its absolute position i_r
@@ -248,8 +248,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   const int tok0 = a.st.cu[s];
   const int n = a.st.cu[s + 1] - tok0;
   const int bp = min(a.block, n);
-  const int c0 = (c - a.st.ch_off[s]) * kScoreChunk;
-  const int c1 = min(c0 + kScoreChunk, n);
+  const int c0 = (c - a.st.ch_off[s]) * a.st.ch_len;
+  const int c1 = min(c0 + a.st.ch_len, n);
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, lr = lane & 31, lh = lane >> 5;
   const int r = 32 * w + lr;
   const int G = a.hq / a.hkv;
@@ -272,7 +272,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   }
   bf16x8 qf[D / 16];
   load_qhat<D>(a, tok0, n, h, r, lh, qf);
-  for (int i = tid; i < kScoreChunk; i += kThreads) acc_s[i] = 0.f;
+  for (int i = tid; i < a.st.ch_len; i += kThreads) acc_s[i] = 0.f;
 
   // keys [c0 - 128, c0) are recomputed for the diagonals owned by this chunk
   const int kstart = max(c0 - 128, 0);
