@@ -286,6 +286,150 @@ __global__ __launch_bounds__(1024) void sel_tie(SelectArgs a) {
   }
 }
 
+// Short problems: every selection problem of the call in one 1024-thread workgroup, the
+// three radix passes through an LDS histogram and the lowest-id tie break in the same
+// launch -- one launch instead of the seven above, the same threshold key, counts and
+// tie cut (every sum is an exact integer, so the result does not depend on the path).
+constexpr int kSmallUnits = 16384;    // largest problem (units) taken by sel_small
+
+__global__ __launch_bounds__(1024) void sel_small(SelectArgs a) {
+  __shared__ uint32_t cnt[kHistBuckets];
+  __shared__ unsigned long long mass[kHistBuckets];
+  __shared__ unsigned long long smass[1024];
+  __shared__ uint32_t scnt[1024];
+  __shared__ SelState sS;
+  __shared__ uint32_t wcount[16];
+  __shared__ int found;
+  const int p = blockIdx.x, tid = threadIdx.x;
+  SelState S = a.sel[p];
+  if (S.mode != 0) return;                // the same decision in every thread
+  const Problem pr = problem_of(a, p);
+  const int top = kHistBuckets - 2 * tid; // thread t owns buckets [top - 2, top): thread
+                                          // order is descending key order
+#pragma unroll 1
+  for (int pass = 0; pass < 3; ++pass) {
+    const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
+    const uint32_t dmask = pass == 2 ? 1023u : 2047u;
+    for (int b = tid; b < kHistBuckets; b += 1024) {
+      cnt[b] = 0u;
+      mass[b] = 0ull;
+    }
+    if (tid == 0) sS = S;
+    __syncthreads();
+    for (int i = tid; i < S.n; i += 1024) {
+      const float x = pr.scores[i];
+      const uint32_t key = __float_as_uint(x);
+      const bool match = pass == 0 || (pass == 1 && (key >> 21) == (S.prefix >> 21)) ||
+                         (pass == 2 && (key >> 10) == (S.prefix >> 10));
+      if (match) {
+        const uint32_t dg = (key >> shift) & dmask;
+        atomicAdd(&cnt[dg], 1u);
+        atomicAdd(&mass[dg], to_fx(x));
+      }
+    }
+    __syncthreads();
+    unsigned long long bm[2];
+    uint32_t bc[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      bm[i] = mass[top - 1 - i];
+      bc[i] = cnt[top - 1 - i];
+    }
+    const unsigned long long lm = bm[0] + bm[1];
+    const uint32_t lc = bc[0] + bc[1];
+    // inclusive scan over the threads (Hillis-Steele, integers: exact and order-free)
+    smass[tid] = lm;
+    scnt[tid] = lc;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+      const unsigned long long vm = tid >= off ? smass[tid - off] : 0ull;
+      const uint32_t vc = tid >= off ? scnt[tid - off] : 0u;
+      __syncthreads();
+      smass[tid] += vm;
+      scnt[tid] += vc;
+      __syncthreads();
+    }
+    const unsigned long long excl_m = smass[tid] - lm;
+    const uint32_t excl_c = scnt[tid] - lc;
+    if (pass == 0) {
+      const unsigned long long total = smass[1023];
+      S.total = total;
+      if (total == 0ull) {
+        S.mode = 1;
+      } else {
+        double t = ceil((double)a.gamma * (double)total);
+        unsigned long long thr = (unsigned long long)t;
+        if (thr < 1ull) thr = 1ull;
+        if (thr > total) S.mode = 1;      // never reached: take every unit
+        S.thr = thr;
+      }
+      if (S.mode == 1) {                  // the same in every thread
+        S.key = 0u;
+        S.idcut = 0x7FFFFFFF;
+        S.k = S.n;
+        if (tid == 0) a.sel[p] = S;
+        return;
+      }
+      if (tid == 0) sS = S;
+      __syncthreads();
+    }
+    unsigned long long run = S.mass_above + excl_m;
+    uint32_t runc = S.cnt_above + excl_c;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      if (run < S.thr && run + bm[i] >= S.thr) {   // exactly one bucket of all threads
+        SelState T = S;
+        const uint32_t digit = (uint32_t)(top - 1 - i);
+        T.prefix |= digit << shift;
+        T.mass_above = run;
+        T.cnt_above = runc;
+        if (pass == 2) {
+          T.key = T.prefix;
+          T.n_eq = bc[i];
+          const unsigned long long f = bm[i] / bc[i];   // equal keys carry equal mass
+          const unsigned long long need = (T.thr - run + f - 1) / f;
+          T.need_eq = (uint32_t)need;
+          T.k = (int32_t)(runc + need);
+          T.idcut = (need >= bc[i]) ? 0x7FFFFFFF : -1;
+        }
+        sS = T;
+      }
+      run += bm[i];
+      runc += bc[i];
+    }
+    __syncthreads();
+    S = sS;
+    __syncthreads();                      // every thread has read sS before it is reused
+  }
+  // lowest-id tie break (as sel_tie), when some but not all units of the key are taken
+  if (S.idcut == -1) {
+    const int w = tid >> 6, lane = tid & 63;
+    uint32_t running = 0;
+    if (tid == 0) found = -1;
+    __syncthreads();
+    for (int base = 0; base < S.n; base += 1024) {
+      const int i = base + tid;
+      const bool f = i < S.n && __float_as_uint(pr.scores[i]) == S.key;
+      const unsigned long long bal = __ballot(f);
+      if (lane == 0) wcount[w] = (uint32_t)__popcll(bal);
+      __syncthreads();
+      uint32_t before = 0, chunk = 0;
+      for (int k = 0; k < 16; ++k) {
+        if (k < w) before += wcount[k];
+        chunk += wcount[k];
+      }
+      const uint32_t rank = running + before + (uint32_t)__popcll(bal & __lanemask_lt());
+      if (f && rank + 1 == S.need_eq) found = i;
+      __syncthreads();
+      if (found >= 0) break;
+      running += chunk;
+      __syncthreads();
+    }
+    S.idcut = found;
+  }
+  if (tid == 0) a.sel[p] = S;
+}
+
 // ---------------------------------------------------------------- conversion to lists
 
 // Vertical-slash heads: mark, per key block / block diagonal, what the selected lines
@@ -813,13 +957,17 @@ hipError_t launch_select_pipeline(const SelectArgs &a, hipStream_t stream) {
   if (a.vs_granularity == 1)
     hipLaunchKernelGGL(pool_lines, dim3((a.nb_total + 3) / 4, a.hq), dim3(256), 0, stream, a);
   hipLaunchKernelGGL(sel_init, dim3(problems), dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(sel_hist<0>, dim3(slices, problems), dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(sel_scan<0>, dim3(problems), dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(sel_hist<1>, dim3(slices, problems), dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(sel_scan<1>, dim3(problems), dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(sel_hist<2>, dim3(slices, problems), dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(sel_scan<2>, dim3(problems), dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(sel_tie, dim3(problems), dim3(1024), 0, stream, a);
+  if (max_units <= kSmallUnits) {
+    hipLaunchKernelGGL(sel_small, dim3(problems), dim3(1024), 0, stream, a);
+  } else {
+    hipLaunchKernelGGL(sel_hist<0>, dim3(slices, problems), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(sel_scan<0>, dim3(problems), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(sel_hist<1>, dim3(slices, problems), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(sel_scan<1>, dim3(problems), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(sel_hist<2>, dim3(slices, problems), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(sel_scan<2>, dim3(problems), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(sel_tie, dim3(problems), dim3(1024), 0, stream, a);
+  }
   {
     int max_n = 0;
     for (int s = 0; s < a.st.n_seq; ++s) max_n = max(max_n, a.st.cu[s + 1] - a.st.cu[s]);
