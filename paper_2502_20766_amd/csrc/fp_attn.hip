@@ -936,24 +936,23 @@ hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t stream) {
     return (int)std::min<int64_t>((wg_per_cu * cus / 8) * 8, (total + 7) / 8 * 8);
   };
   // groups interleaved on an XCD when there are at most kMixItems items per workgroup
-  AttnArgs b = a;
-  b.mix = total <= (int64_t)kMixItems * grid(a.block == 128 ? Geo<128>::WG_PER_CU
-                                                             : Geo<64>::WG_PER_CU);
-  const AttnArgs &a2 = b;
+  AttnArgs args = a;
+  args.mix = total <= (int64_t)kMixItems * grid(a.block == 128 ? Geo<128>::WG_PER_CU
+                                                                : Geo<64>::WG_PER_CU);
   if (a.block == 128) {
     if (a.d == 128)
       hipLaunchKernelGGL((sparse_fa_fwd<128, 128>), dim3(grid(Geo<128>::WG_PER_CU)),
-                         dim3(Geo<128>::THREADS), 0, stream, a2);
+                         dim3(Geo<128>::THREADS), 0, stream, args);
     else
       hipLaunchKernelGGL((sparse_fa_fwd<64, 128>), dim3(grid(Geo<128>::WG_PER_CU)),
-                         dim3(Geo<128>::THREADS), 0, stream, a2);
+                         dim3(Geo<128>::THREADS), 0, stream, args);
   } else {
     if (a.d == 128)
       hipLaunchKernelGGL((sparse_fa_fwd<128, 64>), dim3(grid(Geo<64>::WG_PER_CU)),
-                         dim3(Geo<64>::THREADS), 0, stream, a2);
+                         dim3(Geo<64>::THREADS), 0, stream, args);
     else
       hipLaunchKernelGGL((sparse_fa_fwd<64, 64>), dim3(grid(Geo<64>::WG_PER_CU)),
-                         dim3(Geo<64>::THREADS), 0, stream, a2);
+                         dim3(Geo<64>::THREADS), 0, stream, args);
   }
   return hipGetLastError();
 }
