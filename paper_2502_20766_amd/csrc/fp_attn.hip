@@ -15,8 +15,11 @@
 //     lane owns one query row and half of the stage's keys: the row max needs one lane
 //     swap.  K rows are read with bits 2 and 3 of the row index swapped, which makes the
 //     keys a lane holds in S^T exactly the 8 consecutive keys its P^T B-operand needs;
-//   * online softmax in the log2 domain (exp2 with log2(e) folded into the scale), the
-//     O rescale skipped when no row of the wave sees a new maximum;
+//   * online softmax in the log2 domain (exp2 with log2(e) folded into the scale); a row's
+//     reference max moves (with the O rescale) only when a score rises more than 2^8 in
+//     weight terms above it, so most stages skip the rescale;
+//   * the two LDS stage buffers alternate within each key block (every row takes an even
+//     number of stages), so the unrolled stage pair reads them at constant offsets;
 //   * O^T += V^T P^T on the same MFMA, and O^T keeps one query row per lane, so the
 //     rescale by exp2(m_old - m_new) is per lane.
 // A persistent grid walks each KV group's (sequence, query head, query block) items in a
@@ -214,6 +217,7 @@ struct Row {
 
 constexpr int kChunk = 16;   // consecutive ordered items kept together on one XCD
 constexpr int kMixItems = 8;    // at most this many items per workgroup: groups interleaved
+constexpr float kLazyLog2 = 8.f;  // rise of a row's max (log2 units) that moves its reference
 
 // Item v of XCD x's work queue -> (KV group g, index j into g's ordered items), false once
 // the queue is exhausted (every later v is then exhausted too).
@@ -354,6 +358,8 @@ void sparse_fa_fwd(AttnArgs a) {
   const int lh = lane >> 5;
   const int qrow = 32 * w + lr;           // this lane's query row within the block
   const float c = a.scale_log2;
+  // a rise of kLazyLog2 in log2 units, in raw logit units (c > 0; clamped to stay finite)
+  const float lazy_raw = fminf(kLazyLog2 / c, 3.0e38f);
   const int64_t kv_row = (int64_t)a.hkv * D;  // elements between consecutive tokens
 
   // a row from its item record {packed (s, kk, I), blocks, first block, second block}
@@ -517,9 +523,8 @@ void sparse_fa_fwd(AttnArgs a) {
     cur = next_row();
     nxt_valid = 0;
   }
-  int buf = 0;
   int k0_next = stage_first_key<B>(cur, cur.J0, 0);
-  if (k0_next >= 0) issue(cur, k0_next, buf);
+  if (k0_next >= 0) issue(cur, k0_next, 0);
   bf16x8 qf[KS];
   while (true) {
     // ---- row setup: Q^T fragments (lane owns query row q0 + qrow), zero state
@@ -540,115 +545,131 @@ void sparse_fa_fwd(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < DB; ++i) oacc[i] = f32x16{};
     float m_ref = -INFINITY;   // reference max (raw logit units) of this lane's row
+    float mc = 0.f;             // m_ref * c (0 while m_ref is -inf)
+    float m_trig = -INFINITY;   // m_ref + lazy_raw: a score above it moves the reference
     float l_run = 0.f;          // this lane's share of the row sum of the bf16 weights
     int J_cur = cur.J0;         // block of the stage being prefetched
     int J_pre = cur.J1;         // block after it
-    // stage t covers keys J*128 + 64*(t&1) .. +63 of block J = list[t >> 1]; a row with no
-    // blocks still takes one (empty) stage so that its zero output is written
-    const int n_stages = max(2 * cur.cnt, 1);
-    for (int t = 0; t < n_stages; ++t) {
+    // stage t covers keys J*B + (B/2)*(t&1) .. of block J = list[t >> 1]; a row with no
+    // blocks still takes two (empty) stages so that its zero output is written.  Every row
+    // has an even number of stages, so even stages read LDS buffer 0 and odd ones buffer 1,
+    // and each buffer's read offsets are constants of the unrolled pair.
+    const int n_stages = 2 * max(cur.cnt, 1);
+    auto stage = [&](auto cbc, const int t) {
+      constexpr int CB = decltype(cbc)::value;   // LDS buffer of this stage's K/V tiles
       const int k0 = k0_next;
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's DMA of stage t landed
       barrier();                        // ... and every wave's; stage t-1 reads are done
       fetch_step();
       // the next stage is the row's next one, or the first stage of the next row
       k0_next = -1;
-      if (t + 1 < 2 * cur.cnt) {
-        if ((t & 1) == 0) {
+      if (t + 1 < n_stages) {
+        if constexpr (CB == 0) {
           k0_next = stage_first_key<B>(cur, J_cur, 1);
         } else {
           J_cur = J_pre;
           J_pre = ((t >> 1) + 2 < cur.cnt) ? cur.list[(t >> 1) + 2] : -1;
           k0_next = stage_first_key<B>(cur, J_cur, 0);
         }
-        if (k0_next >= 0) issue(cur, k0_next, buf ^ 1);
+        if (k0_next >= 0) issue(cur, k0_next, CB ^ 1);
       } else {
         fetch_finish();
         if (nxt_valid) {
           const Row nr = next_row();
           k0_next = stage_first_key<B>(nr, nr.J0, 0);
-          if (k0_next >= 0) issue(nr, k0_next, buf ^ 1);
+          if (k0_next >= 0) issue(nr, k0_next, CB ^ 1);
         }
       }
-      buf ^= 1;
-      if (k0 < 0) continue;
-
-    const int kq = k0 - q0;             // key offset relative to the query block start
-    const bool diag = kq >= 0;          // diagonal block: keys after the query are masked
-    uint32_t ka[KS];                    // this stage's K fragment LDS addresses (sub-block 0)
+      if (k0 < 0) return;
+      const int kq = k0 - q0;             // key offset relative to the query block start
+      const bool diag = kq >= 0;          // diagonal block: keys after the query are masked
+      uint32_t ka[KS];                    // this stage's K fragment LDS addresses (sub-block 0)
 #pragma unroll
-    for (int k = 0; k < KS; ++k) ka[k] = lds_base + (buf ^ 1) * 2 * S::BYTES + kaddr_rel[k];
-    f32x16 sacc[2];
-    auto qk_block = [&](auto b2c) {
-      constexpr int b2 = decltype(b2c)::value;
-      sacc[b2] = f32x16{};
-      bf16x8 kf[KS];            // all K fragments in flight before the first MFMA
+      for (int k = 0; k < KS; ++k) ka[k] = lds_base + CB * 2 * S::BYTES + kaddr_rel[k];
+      f32x16 sacc[2];
+      auto qk_block = [&](auto b2c) {
+        constexpr int b2 = decltype(b2c)::value;
+        sacc[b2] = f32x16{};
+        bf16x8 kf[KS];            // all K fragments in flight before the first MFMA
 #pragma unroll
-      for (int k = 0; k < KS; ++k)
-        kf[k] = *reinterpret_cast<const bf16x8 *>(lds + (ka[k] - lds_base) + b2 * 32 * S::RB);
+        for (int k = 0; k < KS; ++k)
+          kf[k] = *reinterpret_cast<const bf16x8 *>(lds + (ka[k] - lds_base) + b2 * 32 * S::RB);
 #pragma unroll
-      for (int k = 0; k < KS; ++k)
-        sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[k], qf[k], sacc[b2], 0, 0, 0);
-    };
-    // Move the reference max when some row of the wave sees a new maximum (rare after the
-    // first blocks), rescaling O and the row sums.
-    auto update_max = [&](float mt) {
-      const float m_new = fmaxf(m_ref, mt);
-      if (__ballot(m_new > m_ref)) {
-        const float alpha = __builtin_amdgcn_exp2f((m_ref - m_new) * c);
-        const float a2 = (m_ref == m_new) ? 1.f : alpha;
-        l_run *= a2;
+        for (int k = 0; k < KS; ++k)
+          sacc[b2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[k], qf[k], sacc[b2], 0, 0, 0);
+      };
+      // Move the reference max, rescaling O and the row sums, only when some row of the wave
+      // sees a score more than kLazyLog2 (log2 units) above it; smaller rises keep the old
+      // reference, so weights stay below 2^kLazyLog2 (bf16 and the float32 sums hold them
+      // with the same relative precision as weights below 1) and most stages skip the
+      // rescale.  While a row's reference is -inf its trigger is -inf too, so its first
+      // visible score moves it; a row with no visible key keeps -inf (weights 0).  `mt` is
+      // this lane's max over its half of the row's stage keys: the two lanes of a row share
+      // the trigger, so the wave-wide vote needs no exchange, and only a moving reference
+      // takes the row max across the lane pair.
+      auto update_max = [&](float mt) {
+        if (__ballot(mt > m_trig)) {
+          const float m_new = fmaxf(m_ref, wave_pair_max(mt));
+          const float alpha = __builtin_amdgcn_exp2f((m_ref - m_new) * c);
+          const float a2 = (m_ref == m_new) ? 1.f : alpha;
+          l_run *= a2;
 #pragma unroll
-        for (int i = 0; i < DB; ++i) oacc[i] *= a2;
-        m_ref = m_new;
+          for (int i = 0; i < DB; ++i) oacc[i] *= a2;
+          m_ref = m_new;
+          const bool none = m_new == -INFINITY;
+          mc = none ? 0.f : m_new * c;
+          m_trig = none ? -INFINITY : m_new + lazy_raw;
+        }
+      };
+      // ---- O^T += V^T P^T, 16 keys per step; one ds_read_b128 per V^T fragment
+      const uint8_t *vs = lds + (CB * 2 + 1) * S::BYTES + vaddr_rel;
+      auto pv_step = [&](auto tc, const bf16x8 &pf) {
+        constexpr int t = decltype(tc)::value;
+        bf16x8 vf[DB];
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          vf[db] = *reinterpret_cast<const bf16x8 *>(vs + db * 1024 + t * 32 * D);
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db], pf, oacc[db], 0, 0, 0);
+      };
+      // ---- the stage's scores, one running-max update for all its keys, the bf16 weights
+      // (P^T steps of 16 keys) and their sum, then O^T += V^T P^T
+      constexpr int SB = Geo<B>::SUB;
+      qk_block(std::integral_constant<int, 0>{});
+      if constexpr (SB == 2) qk_block(std::integral_constant<int, 1>{});
+      if (diag) {
+#pragma unroll
+        for (int b2 = 0; b2 < SB; ++b2)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int key = kq + b2 * 32 + 16 * (v >> 3) + 8 * lh + (v & 7);
+            if (key > qrow) sacc[b2][v] = -INFINITY;
+          }
       }
-    };
-    // ---- O^T += V^T P^T, 16 keys per step; one ds_read_b128 per V^T fragment
-    const uint8_t *vs = lds + ((buf ^ 1) * 2 + 1) * S::BYTES + vaddr_rel;
-    auto pv_step = [&](auto tc, const bf16x8 &pf) {
-      constexpr int t = decltype(tc)::value;
-      bf16x8 vf[DB];
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-        vf[db] = *reinterpret_cast<const bf16x8 *>(vs + db * 1024 + t * 32 * D);
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db], pf, oacc[db], 0, 0, 0);
-    };
-    // ---- the stage's scores, one running-max update for all its keys, the bf16 weights
-    // (P^T steps of 16 keys) and their sum, then O^T += V^T P^T
-    constexpr int SB = Geo<B>::SUB;
-    qk_block(std::integral_constant<int, 0>{});
-    if constexpr (SB == 2) qk_block(std::integral_constant<int, 1>{});
-    if (diag) {
+      float mt = -INFINITY;
 #pragma unroll
       for (int b2 = 0; b2 < SB; ++b2)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int key = kq + b2 * 32 + 16 * (v >> 3) + 8 * lh + (v & 7);
-          if (key > qrow) sacc[b2][v] = -INFINITY;
-        }
-    }
-    float mt = -INFINITY;
+        for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sacc[b2][v]);
+      update_max(mt);
+      bf16x8 pf[2 * SB];
 #pragma unroll
-    for (int b2 = 0; b2 < SB; ++b2)
+      for (int b2 = 0; b2 < SB; ++b2)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, sacc[b2][v]);
-    update_max(wave_pair_max(mt));
-    const float mc = (m_ref == -INFINITY) ? 0.f : m_ref * c;
-    bf16x8 pf[2 * SB];
-#pragma unroll
-    for (int b2 = 0; b2 < SB; ++b2)
-#pragma unroll
-      for (int v = 0; v < 16; ++v)
-        pf[2 * b2 + (v >> 3)][v & 7] = (__bf16)__builtin_amdgcn_exp2f(fmaf(sacc[b2][v], c, -mc));
-    l_run = sum_weights(pf, l_run);
-    pv_step(std::integral_constant<int, 0>{}, pf[0]);
-    pv_step(std::integral_constant<int, 1>{}, pf[1]);
-    if constexpr (SB == 2) {
-      pv_step(std::integral_constant<int, 2>{}, pf[2]);
-      pv_step(std::integral_constant<int, 3>{}, pf[3]);
-    }
+        for (int v = 0; v < 16; ++v)
+          pf[2 * b2 + (v >> 3)][v & 7] = (__bf16)__builtin_amdgcn_exp2f(fmaf(sacc[b2][v], c, -mc));
+      l_run = sum_weights(pf, l_run);
+      pv_step(std::integral_constant<int, 0>{}, pf[0]);
+      pv_step(std::integral_constant<int, 1>{}, pf[1]);
+      if constexpr (SB == 2) {
+        pv_step(std::integral_constant<int, 2>{}, pf[2]);
+        pv_step(std::integral_constant<int, 3>{}, pf[3]);
+      }
+    };
+    for (int t = 0; t < n_stages; t += 2) {
+      stage(std::integral_constant<int, 0>{}, t);
+      stage(std::integral_constant<int, 1>{}, t + 1);
     }
 
     // ---- normalise and store: lane holds query row qrow, d = 32db + 8(v/4) + 4lh + v%4

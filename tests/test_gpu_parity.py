@@ -2,6 +2,7 @@
 
 Every case goes through the C ABI (Python binding = argument marshalling only)."""
 import math
+import types
 
 import numpy as np
 import pytest
@@ -130,6 +131,52 @@ def test_sparse_attention_empty_rows_and_out_of_range_blocks():
     ref = oracle.sparse_attention_rows(layer.q[:, 0], layer.k[:, 0], layer.v[:, 0], m, 128,
                                        1 / math.sqrt(128), [2])
     assert np.abs(o[256:384, 0] - ref[2]).max() <= O_MAX_ABS
+
+
+def test_sparse_attention_rising_and_jumping_scores():
+    """Scores that rise along a row's key blocks, by less than 8 (log2 units) per block on
+    head 0 and with jumps of 20-40 on head 1, so that the running reference max of the
+    online softmax is kept through small rises (weights above 1) and moved on large ones."""
+    fpx = _fpx()
+    n, d, block = 2048, 128, 128
+    nb = n // block
+    rng = np.random.default_rng(4242)
+    scale = 1.0 / math.sqrt(d)
+    u = np.ones(d) / math.sqrt(d)
+    alpha = 8.0
+    per_unit = alpha * scale / math.log(2.0)     # log2-domain score per unit of beta
+    rises = {0: 2.5 * np.arange(nb),
+             1: np.array([0, 0, 30, 2, 5, 40, 41, 3, 60, 58, 61, 90, 20, 95, 96, 130.0])}
+    q = np.zeros((n, 2, d), np.float32)
+    k = np.zeros((n, 1, d), np.float32)
+    v = rng.standard_normal((n, 1, d)).astype(np.float32)
+    for h in range(2):
+        q[:, h] = alpha * u + 0.05 * rng.standard_normal((n, d))
+    # one KV head: the two query heads see different rises through different Q directions
+    w = rng.standard_normal(d)
+    w -= (w @ u) * u
+    w /= np.linalg.norm(w)
+    q[:, 1] = alpha * w + 0.05 * rng.standard_normal((n, d))
+    for J in range(nb):
+        kb = slice(J * block, (J + 1) * block)
+        k[kb, 0] = ((rises[0][J] / per_unit) * u + (rises[1][J] / per_unit) * w
+                    + 0.3 * rng.standard_normal((block, d)))
+    q, k, v = (synth.round_to_bf16(x) for x in (q, k, v))
+    masks = {(0, 0): np.tril(np.ones((nb, nb), bool))}
+    m1 = np.tril(rng.random((nb, nb)) < 0.5)
+    m1[np.arange(nb), 0] = True
+    m1[np.arange(nb), np.arange(nb)] = True
+    masks[(0, 1)] = m1
+    layer = types.SimpleNamespace(q=q, k=k, v=v, cu_seqlens=np.array([0, n], np.int32),
+                                  spec=types.SimpleNamespace(block=block))
+    qd, kd, vd = to_device(layer)
+    shape = fpx.Shape(layer.cu_seqlens, 2, 1, d)
+    idx = fpx.indices_from_masks(shape, masks, qd.device)
+    o = fpx.sparse_attn(qd, kd, vd, idx)
+    torch.cuda.synchronize()
+    mx, mean = compare_outputs(layer, o.float().cpu().numpy(), masks)
+    log(f"[attn-rising-scores] max_abs {mx:.3e} mean_abs {mean:.3e}")
+    assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
 
 
 # ---------------------------------------------------------------- full path vs oracle
