@@ -48,7 +48,9 @@ __device__ __forceinline__ int k_swz(int chunk, int key) {
 
 // Keys [kt, kt + TK) of KV head g (rows past n are zero), staged through the registers of
 // NT threads: the next tile is loaded while the current one is in use, then stored to LDS
-// swizzled.
+// swizzled.  The loads go through a buffer resource over the tile's rows that ends at the
+// sequence's last key (its range check returns zero past it): the per-thread offset is
+// fixed and the tile and iteration steps are scalar.
 template <int D, int NT = kThreads, int TK = KT>
 struct KTile {
   static constexpr int KCH = D / 8;                     // 16-byte chunks per key
@@ -59,14 +61,20 @@ struct KTile {
   uint4 v[NIT];
   __device__ __forceinline__ void load(const uint16_t *kbase, int64_t kv_row, int kt, int n,
                                        int tid) {
+    const uint64_t p = (uint64_t)(uintptr_t)(kbase + (int64_t)kt * kv_row);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)p);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
+    const int row_bytes = (int)kv_row * 2;
+    const int nrec = __builtin_amdgcn_readfirstlane(min(TK, n - kt) * row_bytes);
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(uintptr_t)(((uint64_t)hi << 32) | lo), (short)0, nrec, 0x00020000);
+    const int voff = (tid / KCH) * row_bytes + (tid % KCH) * 16;
 #pragma unroll
     for (int it = 0; it < NIT; ++it) {
-      const int c = it * NT + tid;
-      if (CH < NT && c >= CH) continue;
-      const int j = kt + c / KCH;
-      v[it] = *reinterpret_cast<const uint4 *>(kbase + (int64_t)min(j, n - 1) * kv_row +
-                                               (c % KCH) * 8);
-      if (j >= n) v[it] = make_uint4(0, 0, 0, 0);
+      if (CH < NT && tid >= CH) continue;
+      const auto x = __builtin_amdgcn_raw_buffer_load_b128(
+          r, voff, __builtin_amdgcn_readfirstlane(it * (NT / KCH) * row_bytes), 0);
+      v[it] = make_uint4(x[0], x[1], x[2], x[3]);
     }
   }
   __device__ __forceinline__ void store(uint16_t *Ks, int tid) const {
@@ -234,12 +242,15 @@ __global__ __launch_bounds__(256) void rep_stats_combine(SelectArgs a) {
 // the barrier-separated phases.
 constexpr int LKT = 32;                        // keys per line-pass tile
 constexpr int LPITCH = LKT + 1;                // odd pitch: diagonal reads are conflict free
+constexpr int LPAD = LKT - 1;                  // zero rows above and below the weight rows
 
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void rep_lines(
     SelectArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][LKT * D];   // double-buffered K tile
-  __shared__ float Pt[128 * LPITCH];           // Â tile, [row][key]
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[LKT * D];   // K tile
+  // Â tile, [row][key], with LPAD zero rows on both sides: every diagonal of the tile is
+  // then LKT reads at fixed offsets (the rows past b' hold zero weights)
+  __shared__ float Pt[(LPAD + 128 + LPAD) * LPITCH];
   __shared__ float acc_s[kScoreChunk];         // owned slash offsets
   __shared__ float red[4][LKT];                // per wave: column sums of the tile
   const int c = blockIdx.x;
@@ -273,23 +284,27 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   bf16x8 qf[D / 16];
   load_qhat<D>(a, tok0, n, h, r, lh, qf);
   for (int i = tid; i < a.st.ch_len; i += kThreads) acc_s[i] = 0.f;
+  for (int i = tid; i < LPAD * LPITCH; i += kThreads) {
+    Pt[i] = 0.f;
+    Pt[(LPAD + 128) * LPITCH + i] = 0.f;
+  }
 
   // keys [c0 - 128, c0) are recomputed for the diagonals owned by this chunk
   const int kstart = max(c0 - 128, 0);
-  // two barriers per tile: after the weights (the next K tile is then stored into the other
-  // buffer, whose last reader finished a tile ago) and after the diagonal pass
+  // two barriers per tile: after the weights (every wave's K reads are then done, so the
+  // next K tile, already in registers, is stored over the current one) and after the
+  // diagonal pass
   KTile<D, kThreads, LKT> tile;
   tile.load(kbase, kv_row, kstart, n, tid);
-  tile.store(Ks[0], tid);
+  tile.store(Ks, tid);
   if (kstart + LKT < c1) tile.load(kbase, kv_row, kstart + LKT, n, tid);
   __syncthreads();
-  int buf = 0;
   for (int kt = kstart; kt < c1; kt += LKT) {
     f32x16 sacc = {};
 #pragma unroll
     for (int k = 0; k < D / 16; ++k) {
       const bf16x8 kf =
-          *reinterpret_cast<const bf16x8 *>(Ks[buf] + lr * D + k_swz<D>(2 * k + lh, lr) * 8);
+          *reinterpret_cast<const bf16x8 *>(Ks + lr * D + k_swz<D>(2 * k + lh, lr) * 8);
       sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[k], kf, sacc, 0, 0, 0);
     }
     // masking only in tiles that reach past the sequence or the first row's position, or
@@ -304,7 +319,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         float p = __builtin_amdgcn_exp2f(sacc[v] * sl2 - rm[v]);
         if constexpr (decltype(masked)::value)
           p = ((j < n) & (j <= n - bp + rv) & (rv < bp)) ? p : 0.f;
-        Pt[rv * LPITCH + lr] = p;
+        Pt[(LPAD + rv) * LPITCH + lr] = p;
         cs += p;
       }
     };
@@ -319,27 +334,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     }
     __syncthreads();
     if (kt + LKT < c1) {
-      tile.store(Ks[buf ^ 1], tid);
+      tile.store(Ks, tid);
       if (kt + 2 * LKT < c1) tile.load(kbase, kv_row, kt + 2 * LKT, n, tid);   // next-next tile
     }
     // slash lines: diagonal o with last-row key jl = n - 1 - o meets this tile for
-    // jl in [kt, kt + LKT + bp - 1); rows r with key jl - (bp - 1) + r inside the tile
+    // jl in [kt, kt + LKT + bp - 1); its element in row rr is key jl - (bp - 1) + rr - kt,
+    // so starting from row rr0 = bp - 1 - (jl - kt) (which may lie in the zero rows) it is
+    // LKT elements at stride LPITCH + 1; eight partial sums in a fixed order
     const int jl = kt + tid;
     if (tid < LKT + bp - 1 && jl >= c0 && jl < c1) {
-      const int rlo = max(0, bp - 1 - (jl - kt));
-      const int rhi = min(bp, bp - 1 - (jl - kt) + LKT);
-      // element (rr, jl - (bp - 1) + rr - kt) of the tile: stride LPITCH + 1 along rr;
-      // eight partial sums keep eight LDS reads in flight (fixed order: deterministic)
-      const float *dp = Pt + (jl - (bp - 1) - kt) + rlo * (LPITCH + 1);
-      const int len = rhi - rlo;
+      const float *dp = Pt + (LPAD + bp - 1 - (jl - kt)) * LPITCH;
       float d[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      int i = 0;
-      for (; i + 8 <= len; i += 8)
+#pragma unroll
+      for (int i = 0; i < LKT; i += 8)
 #pragma unroll
         for (int u = 0; u < 8; ++u) d[u] += dp[(i + u) * (LPITCH + 1)];
-#pragma unroll
-      for (int u = 0; u < 7; ++u)
-        if (i + u < len) d[u] += dp[(i + u) * (LPITCH + 1)];
       const float ds = ((d[0] + d[1]) + (d[2] + d[3])) + ((d[4] + d[5]) + (d[6] + d[7]));
       acc_s[jl - c0] += ds;
     }
@@ -350,7 +359,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
             ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
     }
     __syncthreads();
-    buf ^= 1;
   }
   for (int i = tid; i < c1 - c0; i += kThreads) {
     const int jl = c0 + i;
