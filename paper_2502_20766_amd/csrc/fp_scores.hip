@@ -416,7 +416,9 @@ hipError_t launch_rep_scores(const SelectArgs &a, hipStream_t stream) {
   dim3 grid(ch_total, a.hq);
   // 4 (or 2) query heads of one KV group per workgroup when the group size allows
   const int G = a.hq / a.hkv;
-  const int hg = G % 4 == 0 ? 4 : (G % 2 == 0 ? 2 : 1);
+  int hg = G % 4 == 0 ? 4 : (G % 2 == 0 ? 2 : 1);
+  // short problems: fewer heads per workgroup, so that the grid still covers the GPU
+  while (hg > 1 && (int64_t)ch_total * (a.hq / hg) < 512) hg /= 2;
   const dim3 grid_g(ch_total, a.hq / hg), block_g(kThreads * hg);
   if (a.d == 128) {
     if (hg == 4) hipLaunchKernelGGL((rep_stats<128, 4>), grid_g, block_g, 0, stream, a);
