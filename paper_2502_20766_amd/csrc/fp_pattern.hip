@@ -225,13 +225,26 @@ __global__ __launch_bounds__(kLogitThreads) void qa_logits(SelectArgs a) {
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, lr = lane & 31, lh = lane >> 5;
   // stage the rows (rows past the sequence's last block are clamped; their logits are not
   // written)
-  for (int i = tid; i < QT * (D / 4); i += kLogitThreads) {
+  // (every load is issued before the first store, so the loads overlap)
+  constexpr int NST = QT * (D / 4) / kLogitThreads;
+  static_assert(NST * kLogitThreads == QT * (D / 4), "staging covers the tile exactly");
+  float4 qv4[NST], kv4[NST];
+#pragma unroll
+  for (int u = 0; u < NST; ++u) {
+    const int i = tid + u * kLogitThreads;
     const int row = i / (D / 4), c = i % (D / 4);
     const int I = min(TI * QT + row, nb - 1), J = min(TJ * QT + row, nb - 1);
-    *reinterpret_cast<float4 *>(Qs + row * P + 4 * c) = reinterpret_cast<const float4 *>(
+    qv4[u] = reinterpret_cast<const float4 *>(
         a.qbar + ((int64_t)(a.st.nb_off[s] + I) * a.hq + h) * D)[c];
-    *reinterpret_cast<float4 *>(Ks + row * P + 4 * c) = reinterpret_cast<const float4 *>(
+    kv4[u] = reinterpret_cast<const float4 *>(
         a.kbar + ((int64_t)(a.st.nb_off[s] + J) * a.hkv + g) * D)[c];
+  }
+#pragma unroll
+  for (int u = 0; u < NST; ++u) {
+    const int i = tid + u * kLogitThreads;
+    const int row = i / (D / 4), c = i % (D / 4);
+    *reinterpret_cast<float4 *>(Qs + row * P + 4 * c) = qv4[u];
+    *reinterpret_cast<float4 *>(Ks + row * P + 4 * c) = kv4[u];
   }
   __syncthreads();
   const int i0 = 32 * (w >> 2), j0 = 32 * (w & 3);          // block within the tile

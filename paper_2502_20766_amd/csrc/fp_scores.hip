@@ -271,15 +271,19 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   // Â[r, j] = exp2(s_rj * sl2 - m_r) / (l_r * b') = exp2(s_rj * sl2 - m_r - log2(l_r * b')).
   // Lane (lr, lh) holds key lr of the tile for the 16 rows rv(v) = 32 w + 8 (v / 4) + 4 lh
   // + v % 4.
+  // (the 16 row statistics are loaded unconditionally, rows past b' clamped, so that the
+  // loads are in flight together)
   float rm[16];
+  float2 rst[16];
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int rv = 32 * w + 8 * (v >> 2) + 4 * lh + (v & 3);
-    rm[v] = 0.f;
-    if (rv < bp) {
-      const float2 st = a.row_stats[((int64_t)s * a.hq + h) * a.block + rv];
-      rm[v] = st.x + __builtin_amdgcn_logf(st.y * (float)bp);
-    }
+    rst[v] = a.row_stats[((int64_t)s * a.hq + h) * a.block + min(rv, bp - 1)];
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int rv = 32 * w + 8 * (v >> 2) + 4 * lh + (v & 3);
+    rm[v] = rv < bp ? rst[v].x + __builtin_amdgcn_logf(rst[v].y * (float)bp) : 0.f;
   }
   bf16x8 qf[D / 16];
   load_qhat<D>(a, tok0, n, h, r, lh, qf);
