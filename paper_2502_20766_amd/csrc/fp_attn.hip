@@ -828,8 +828,8 @@ __device__ __forceinline__ void sort_slots(unsigned long long *key) {
 }
 
 // Locality order of one KV group's items (s, head, I): ascending by
-//   [1023 - min(blocks / 4, 1023)] [first three listed blocks after block 0] [item id],
-// i.e. longest first in buckets of 4 blocks, and inside a bucket items whose lists start
+//   [1023 - min(blocks / 2, 1023)] [first three listed blocks after block 0] [item id],
+// i.e. longest first in buckets of 2 blocks, and inside a bucket items whose lists start
 // alike are adjacent, so that the items running at the same time on an XCD read the same
 // K/V tiles through its L2.  Item id = row * G + kk (heads of a row adjacent).  Also resets
 // the queue counters.
@@ -866,7 +866,7 @@ __device__ __forceinline__ void sort_group_items(const SeqTable &st, const int32
       unsigned long long e[3];
 #pragma unroll
       for (int t = 0; t < 3; ++t) e[t] = cnt > t + 1 ? min((unsigned)l[t + 1], 0x1FFFu) : 0x1FFFu;
-      const unsigned long long bucket = (unsigned long long)min(cnt >> 2, 1023);
+      const unsigned long long bucket = (unsigned long long)min(cnt >> 1, 1023);
       kv = ((1023ull - bucket) << 53) | (e[0] << 40) | (e[1] << 27) | (e[2] << 14) |
            (unsigned long long)id;
       if (stash)
