@@ -76,6 +76,48 @@ __device__ __forceinline__ Problem problem_of(const SelectArgs &a, int p) {
   return pr;
 }
 
+// Inclusive scan, in thread order over the workgroup, of a (fixed-point mass, count) pair
+// per thread, and the workgroup totals: a scan inside each wave through lane shuffles, then
+// the NW wave totals through `wm`/`wc` (one barrier; the caller separates reuses of them
+// by another).  Integer additions: the result does not depend on their order.
+template <int NW>
+__device__ __forceinline__ void block_incl_scan(unsigned long long &m, uint32_t &c,
+                                                unsigned long long *wm, uint32_t *wc,
+                                                unsigned long long &tot_m, uint32_t &tot_c) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const unsigned long long vm = __shfl_up(m, off);
+    const uint32_t vc = __shfl_up(c, off);
+    if (lane >= off) {
+      m += vm;
+      c += vc;
+    }
+  }
+  if (lane == 63) {
+    wm[w] = m;
+    wc[w] = c;
+  }
+  __syncthreads();
+  unsigned long long before_m = 0ull;
+  uint32_t before_c = 0u;
+  tot_m = 0ull;
+  tot_c = 0u;
+#pragma unroll
+  for (int k = 0; k < NW; ++k) {
+    const unsigned long long x = wm[k];
+    const uint32_t y = wc[k];
+    if (k < w) {
+      before_m += x;
+      before_c += y;
+    }
+    tot_m += x;
+    tot_c += y;
+  }
+  m += before_m;
+  c += before_c;
+}
+
 __device__ __forceinline__ bool is_selected(const SelState &S, float x, int id) {
   const uint32_t key = __float_as_uint(x);
   return key > S.key || (key == S.key && id <= S.idcut);
@@ -159,9 +201,8 @@ __global__ __launch_bounds__(256) void sel_hist(SelectArgs a) {
 // owns buckets [2048 - 8(t+1), 2048 - 8t), so thread order is descending key order.
 template <int PASS>
 __global__ __launch_bounds__(256) void sel_scan(SelectArgs a) {
-  __shared__ unsigned long long smass[256];
-  __shared__ uint32_t scnt[256];
-  __shared__ unsigned long long s_total;
+  __shared__ unsigned long long wmass[4];
+  __shared__ uint32_t wcnt[4];
   const int p = blockIdx.x, tid = threadIdx.x;
   SelState S = a.sel[p];
   if (S.mode != 0) return;
@@ -179,22 +220,11 @@ __global__ __launch_bounds__(256) void sel_scan(SelectArgs a) {
     lm += bm[i];
     lc += bc[i];
   }
-  // inclusive scan over threads (Hillis-Steele, integers: exact and order-free)
-  smass[tid] = lm;
-  scnt[tid] = lc;
-  __syncthreads();
-  for (int off = 1; off < 256; off <<= 1) {
-    const unsigned long long vm = tid >= off ? smass[tid - off] : 0ull;
-    const uint32_t vc = tid >= off ? scnt[tid - off] : 0u;
-    __syncthreads();
-    smass[tid] += vm;
-    scnt[tid] += vc;
-    __syncthreads();
-  }
-  const unsigned long long excl_m = smass[tid] - lm;
-  const uint32_t excl_c = scnt[tid] - lc;
-  if (tid == 255) s_total = smass[255];
-  __syncthreads();
+  unsigned long long im = lm, s_total;
+  uint32_t ic = lc, s_count;
+  block_incl_scan<4>(im, ic, wmass, wcnt, s_total, s_count);
+  const unsigned long long excl_m = im - lm;
+  const uint32_t excl_c = ic - lc;
   if (PASS == 0) {
     const unsigned long long total = s_total;
     S.total = total;
@@ -295,8 +325,8 @@ constexpr int kSmallUnits = 16384;    // largest problem (units) taken by sel_sm
 __global__ __launch_bounds__(1024) void sel_small(SelectArgs a) {
   __shared__ uint32_t cnt[kHistBuckets];
   __shared__ unsigned long long mass[kHistBuckets];
-  __shared__ unsigned long long smass[1024];
-  __shared__ uint32_t scnt[1024];
+  __shared__ unsigned long long wmass[16];
+  __shared__ uint32_t wcnt[16];
   __shared__ SelState sS;
   __shared__ uint32_t wcount[16];
   __shared__ int found;
@@ -337,22 +367,13 @@ __global__ __launch_bounds__(1024) void sel_small(SelectArgs a) {
     }
     const unsigned long long lm = bm[0] + bm[1];
     const uint32_t lc = bc[0] + bc[1];
-    // inclusive scan over the threads (Hillis-Steele, integers: exact and order-free)
-    smass[tid] = lm;
-    scnt[tid] = lc;
-    __syncthreads();
-    for (int off = 1; off < 1024; off <<= 1) {
-      const unsigned long long vm = tid >= off ? smass[tid - off] : 0ull;
-      const uint32_t vc = tid >= off ? scnt[tid - off] : 0u;
-      __syncthreads();
-      smass[tid] += vm;
-      scnt[tid] += vc;
-      __syncthreads();
-    }
-    const unsigned long long excl_m = smass[tid] - lm;
-    const uint32_t excl_c = scnt[tid] - lc;
+    unsigned long long im = lm, total_m;
+    uint32_t ic = lc, total_c;
+    block_incl_scan<16>(im, ic, wmass, wcnt, total_m, total_c);
+    const unsigned long long excl_m = im - lm;
+    const uint32_t excl_c = ic - lc;
     if (pass == 0) {
-      const unsigned long long total = smass[1023];
+      const unsigned long long total = total_m;
       S.total = total;
       if (total == 0ull) {
         S.mode = 1;
