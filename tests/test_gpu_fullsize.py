@@ -45,7 +45,7 @@ def _check_layer(name, spec, gamma, max_budget=0, qa_mode=0):
     q, k, v = to_device(layer)
     with Timer("device select + attention"):
         idx = fpx.select(q, k, layer.cu_seqlens, gamma, spec.tau, spec.min_budget,
-                         max_budget=max_budget, qa_mode=qa_mode)
+                         block=spec.block, max_budget=max_budget, qa_mode=qa_mode)
         o = fpx.sparse_attn(q, k, v, idx)
         torch.cuda.synchronize()
     g = dict(masks=fpx.masks_from_indices(idx), pattern=idx.pattern.cpu().numpy(),
@@ -70,6 +70,14 @@ def test_fullsize_selection_and_sampled_outputs(case):
     name, key, gamma = case
     spec = synth.SPECS[key]
     _check_layer(name, spec, spec.gamma if gamma is None else gamma)
+
+
+def test_fullsize_block64():
+    """The 128k Llama-shaped layer with key blocks of 64 tokens (up to 2048 blocks per row,
+    twice the attention items of block 128): every block set against the oracle, outputs on
+    sampled query blocks."""
+    spec = synth.SPECS["llama128k"].with_params(block=64)
+    _check_layer("llama3-8b-n131072-block64", spec, spec.gamma)
 
 
 def test_maximum_sequence_length():
