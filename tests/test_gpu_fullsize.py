@@ -36,16 +36,18 @@ CASES = [
 ROWS_PER_HEAD = 64          # first, last and 62 seeded random query blocks
 
 
-def _check_layer(name, spec, gamma, max_budget=0, qa_mode=0):
+def _check_layer(name, spec, gamma, max_budget=0, qa_mode=0, vs_granularity=0):
     import paper_2502_20766_amd as fpx
     log(f"[fullsize] {name}: seqlens={spec.seqlens} hq={spec.hq} hkv={spec.hkv} gamma={gamma} "
-        f"tau={spec.tau} m={spec.min_budget} max_budget={max_budget} qa_mode={qa_mode}")
+        f"tau={spec.tau} m={spec.min_budget} max_budget={max_budget} qa_mode={qa_mode} "
+        f"vs_granularity={vs_granularity}")
     with Timer("generate"):
         layer = synth.make_layer(spec)
     q, k, v = to_device(layer)
     with Timer("device select + attention"):
         idx = fpx.select(q, k, layer.cu_seqlens, gamma, spec.tau, spec.min_budget,
-                         block=spec.block, max_budget=max_budget, qa_mode=qa_mode)
+                         block=spec.block, max_budget=max_budget, qa_mode=qa_mode,
+                         vs_granularity=vs_granularity)
         o = fpx.sparse_attn(q, k, v, idx)
         torch.cuda.synchronize()
     g = dict(masks=fpx.masks_from_indices(idx), pattern=idx.pattern.cpu().numpy(),
@@ -56,7 +58,8 @@ def _check_layer(name, spec, gamma, max_budget=0, qa_mode=0):
     del q, k, v, o
     with Timer("oracle selection, all heads"):
         st = compare_selection(layer, g, gamma, spec.tau, spec.min_budget,
-                               max_budget=max_budget, qa_mode=qa_mode)
+                               max_budget=max_budget, qa_mode=qa_mode,
+                               vs_granularity=vs_granularity)
     log(f"  {st}")
     assert_relaxations_bounded(st)
     with Timer("oracle sampled outputs"):
@@ -78,6 +81,13 @@ def test_fullsize_block64():
     sampled query blocks."""
     spec = synth.SPECS["llama128k"].with_params(block=64)
     _check_layer("llama3-8b-n131072-block64", spec, spec.gamma)
+
+
+def test_fullsize_block_pooled_lines():
+    """The 128k Llama-shaped layer with block-pooled vertical-slash lines (key blocks and
+    offset blocks of lines as the selection units) at gamma 0.9."""
+    spec = synth.SPECS["llama128k"]
+    _check_layer("llama3-8b-n131072-pooled-lines", spec, 0.9, vs_granularity=1)
 
 
 def test_maximum_sequence_length():
