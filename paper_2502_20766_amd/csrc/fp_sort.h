@@ -42,14 +42,19 @@ __device__ __forceinline__ void bitonic_stage(unsigned long long (&k)[E],
       k[e] = take_min ? key_min(k[e], v) : key_max(k[e], v);
     }
   } else {
+    // Position tid * E + e pairs with (tid ^ TX) * E + e.  The exchange is stored
+    // element-major (key e of thread t at e * NT + t), so that the lanes of a wave touch
+    // consecutive words (thread-major order would put adjacent lanes E words apart, all in
+    // the same few LDS banks).
+    constexpr int TX = STRIDE / E;
     __syncthreads();                 // the previous LDS stage's reads are done
 #pragma unroll
-    for (int e = 0; e < E; ++e) lds[tid * E + e] = k[e];
+    for (int e = 0; e < E; ++e) lds[e * NT + tid] = k[e];
     __syncthreads();
     const bool take_min = (((tid * E) & STRIDE) == 0) == (((tid * E) & SIZE) == 0);
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      const unsigned long long v = lds[(tid * E + e) ^ STRIDE];
+      const unsigned long long v = lds[e * NT + (tid ^ TX)];
       k[e] = take_min ? key_min(k[e], v) : key_max(k[e], v);
     }
   }
