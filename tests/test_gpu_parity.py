@@ -133,12 +133,13 @@ def test_sparse_attention_empty_rows_and_out_of_range_blocks():
     assert np.abs(o[256:384, 0] - ref[2]).max() <= O_MAX_ABS
 
 
-def test_sparse_attention_rising_and_jumping_scores():
+@pytest.mark.parametrize("block", [128, 64])
+def test_sparse_attention_rising_and_jumping_scores(block):
     """Scores that rise along a row's key blocks, by less than 8 (log2 units) per block on
     head 0 and with jumps of 20-40 on head 1, so that the running reference max of the
     online softmax is kept through small rises (weights above 1) and moved on large ones."""
     fpx = _fpx()
-    n, d, block = 2048, 128, 128
+    n, d = 2048, 128
     nb = n // block
     rng = np.random.default_rng(4242)
     scale = 1.0 / math.sqrt(d)
@@ -146,7 +147,8 @@ def test_sparse_attention_rising_and_jumping_scores():
     alpha = 8.0
     per_unit = alpha * scale / math.log(2.0)     # log2-domain score per unit of beta
     rises = {0: 2.5 * np.arange(nb),
-             1: np.array([0, 0, 30, 2, 5, 40, 41, 3, 60, 58, 61, 90, 20, 95, 96, 130.0])}
+             1: np.repeat(np.array([0, 0, 30, 2, 5, 40, 41, 3, 60, 58, 61, 90, 20, 95, 96, 130.0]),
+                          128 // block)}
     q = np.zeros((n, 2, d), np.float32)
     k = np.zeros((n, 1, d), np.float32)
     v = rng.standard_normal((n, 1, d)).astype(np.float32)
@@ -170,12 +172,12 @@ def test_sparse_attention_rising_and_jumping_scores():
     layer = types.SimpleNamespace(q=q, k=k, v=v, cu_seqlens=np.array([0, n], np.int32),
                                   spec=types.SimpleNamespace(block=block))
     qd, kd, vd = to_device(layer)
-    shape = fpx.Shape(layer.cu_seqlens, 2, 1, d)
+    shape = fpx.Shape(layer.cu_seqlens, 2, 1, d, block)
     idx = fpx.indices_from_masks(shape, masks, qd.device)
     o = fpx.sparse_attn(qd, kd, vd, idx)
     torch.cuda.synchronize()
     mx, mean = compare_outputs(layer, o.float().cpu().numpy(), masks)
-    log(f"[attn-rising-scores] max_abs {mx:.3e} mean_abs {mean:.3e}")
+    log(f"[attn-rising-scores] block {block} max_abs {mx:.3e} mean_abs {mean:.3e}")
     assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
 
 
@@ -362,6 +364,43 @@ def test_block64_attention_on_oracle_masks(case):
     mx, mean = compare_outputs(layer, o.float().cpu().numpy(), masks)
     log(f"  max_abs {mx:.3e} mean_abs {mean:.3e}")
     assert mx <= O_MAX_ABS and mean <= O_MEAN_ABS
+
+
+def test_block64_edges():
+    """Block 64: a query block with no listed blocks gets zeros beside neighbours that list
+    many; an entry outside a query block's causal range (the next query block's diagonal
+    block, a block past the sequence end) is skipped; the last block is partial."""
+    fpx = _fpx()
+    n, nb = 300, 5      # blocks of 64, the last holding 44 tokens
+    log(f"[b64 edges] n={n}")
+    spec = synth.LayerSpec("b64-edges", (n,), 2, 1, 128, 64, ("vs", "qa"), 4, 0.9, 0.1, 1, 11)
+    layer = synth.make_layer(spec)
+    q, k, v = to_device(layer)
+    shape = fpx.Shape(layer.cu_seqlens, 2, 1, 128, 64)
+    full = np.tril(np.ones((nb, nb), bool))
+    idx = fpx.indices_from_masks(shape, {(0, 0): full, (0, 1): full}, q.device)
+    tri = [I * (I + 1) // 2 for I in range(nb + 1)]
+    # head 0: row 2 [0, 1, 2] -> [3, 1, 2]; row 4 [0, 1, 2, 3, 4] -> [0, 1, 9, 3, 4]
+    idx.kb_idx[tri[2]] = 3
+    idx.kb_idx[tri[4] + 2] = 9
+    # head 1: rows 0 and 3 list nothing (rows 1 and 2 list every block)
+    idx.kb_cnt[nb + 0] = 0
+    idx.kb_cnt[nb + 3] = 0
+    o = fpx.sparse_attn(q, k, v, idx).float().cpu().numpy()
+    assert np.all(o[0:64, 1] == 0.0) and np.all(o[192:256, 1] == 0.0)
+    m0 = full.copy()
+    m0[2, 0] = False
+    m0[4, 2] = False
+    m1 = full.copy()
+    m1[0, :] = False
+    m1[3, :] = False
+    for h, m in ((0, m0), (1, m1)):
+        rows = [I for I in range(nb) if m[I].any()]
+        ref = oracle.sparse_attention_rows(layer.q[:, h], layer.k[:, 0], layer.v[:, 0], m, 64,
+                                           1 / math.sqrt(128), rows)
+        for I in rows:
+            err = np.abs(o[I * 64:min((I + 1) * 64, n), h] - ref[I]).max()
+            assert err <= O_MAX_ABS, (h, I, err)
 
 
 B64_SELECT_CASES = [
