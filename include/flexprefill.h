@@ -119,8 +119,9 @@ fp_status fp_indices_size(const fp_shape *shape, size_t *kb_idx_elems, size_t *k
 
 /* Device workspace bytes needed by fp_select / fp_sparse_attn.  Host only.
  * fp_select: 0 when gamma >= 1 (every causal block is listed without any scoring).
- * fp_sparse_attn: the work order (16 bytes per query head and block), 8 counters, and one
- * transposed copy of V (2 * Hkv * NB * block * d bytes, NB = sum of ceil(n_s / block)),
+ * fp_sparse_attn: the work order (16 bytes per query head and block), 8 counters, one
+ * transposed copy of V (2 * Hkv * NB * block * d bytes, NB = sum of ceil(n_s / block)) and
+ * the work order's sort keys and unsorted records (24 bytes per query head and block),
  * written at the start of every call. */
 fp_status fp_select_workspace_size(const fp_shape *shape, const fp_params *params,
                                    size_t *bytes);

@@ -152,9 +152,13 @@ size_t select_layout(const fp_shape *sh, const Dims &dm, char *base, fp::SelectA
 
 // attention workspace: ordered item records [Hq][NB] int4, 8 queue counters, then the V^T
 // tiles [Hkv][NB][block * d] bf16
+// Attention workspace: ordered item records (16 B per query head and block), 8 queue
+// counters, V^T tiles, and the items' sort keys (8 B) and records in id order (16 B).
 size_t attn_layout(const fp_shape *sh, const Dims &dm) {
-  return align_up(16 * dm.nb_total * sh->num_q_heads) + align_up(8 * sizeof(int32_t)) +
-         align_up(2 * (size_t)dm.nb_total * sh->num_kv_heads * sh->block * sh->head_dim);
+  const size_t items = (size_t)dm.nb_total * sh->num_q_heads;
+  return align_up(16 * items) + align_up(8 * sizeof(int32_t)) +
+         align_up(2 * (size_t)dm.nb_total * sh->num_kv_heads * sh->block * sh->head_dim) +
+         align_up(8 * items) + align_up(16 * items);
 }
 
 fp_status hip_fail(hipError_t e, const char *what) {
@@ -286,6 +290,10 @@ fp_status fp_sparse_attn(const fp_shape *shape, const void *q, const void *k, co
   a.items = (int4 *)ws;
   a.queue = (int32_t *)((char *)ws + align_up(16 * dm.nb_total * shape->num_q_heads));
   a.vt = (uint16_t *)((char *)a.queue + align_up(8 * sizeof(int32_t)));
+  a.sort_keys = (unsigned long long *)((char *)a.vt +
+                                       align_up(2 * (size_t)dm.nb_total * shape->num_kv_heads *
+                                                shape->block * shape->head_dim));
+  a.sort_recs = (int4 *)((char *)a.sort_keys + align_up(8 * dm.nb_total * shape->num_q_heads));
   hipError_t e = fp::launch_sparse_attn(a, (hipStream_t)stream);
   return e == hipSuccess ? FP_OK : hip_fail(e, "fp_sparse_attn");
 }

@@ -811,15 +811,17 @@ __global__ void build_item_order_plain(SeqTable st, const int32_t *kb_idx, const
 constexpr int kSortItems = 16384;   // items per KV group sorted in LDS (128 KB of keys)
 constexpr int kSortThreads = 1024;  // threads of a sorting workgroup
 
-// The kSortThreads * E keys in key[] sorted ascending in place: each thread takes E
-// consecutive keys into registers, the bitonic network exchanges them inside the thread,
-// across lanes, and through key[] for strides that cross waves.
+// The n keys at src (device memory) sorted ascending into key[] (kSortThreads * E slots of
+// LDS, the slots past n padded with keys that sort last): each thread takes E consecutive
+// keys into registers, the bitonic network exchanges them inside the thread, across lanes,
+// and through key[] for strides that cross waves.
 template <int E>
-__device__ __forceinline__ void sort_slots(unsigned long long *key) {
+__device__ __forceinline__ void sort_keys(unsigned long long *key, const unsigned long long *src,
+                                          int n) {
   const int tid = threadIdx.x;
   unsigned long long k[E];
 #pragma unroll
-  for (int e = 0; e < E; ++e) k[e] = key[tid * E + e];
+  for (int e = 0; e < E; ++e) k[e] = tid * E + e < n ? src[tid * E + e] : ~0ull;
   bitonic_sort<kSortThreads, E>(k, key, tid);
   __syncthreads();                       // the network's last reads of key[] are done
 #pragma unroll
@@ -827,74 +829,96 @@ __device__ __forceinline__ void sort_slots(unsigned long long *key) {
   __syncthreads();
 }
 
-// Locality order of one KV group's items (s, head, I): ascending by
+// Sort key and item record of item id = row * G + kk of KV group g.  The keys give the
+// locality order of a group's items (s, head, I): ascending by
 //   [1023 - min(blocks / 2, 1023)] [first three listed blocks after block 0] [item id],
 // i.e. longest first in buckets of 2 blocks, and inside a bucket items whose lists start
 // alike are adjacent, so that the items running at the same time on an XCD read the same
-// K/V tiles through its L2.  Item id = row * G + kk (heads of a row adjacent).  Also resets
-// the queue counters.
+// K/V tiles through its L2 (heads of a row adjacent in id).  The list entries are read
+// together, at indices clamped to the row's capacity I + 1.
+__device__ __forceinline__ void item_key(const SeqTable &st, const int32_t *kb_idx,
+                                         const int32_t *kb_cnt, int G, int64_t tri_total, int g,
+                                         int id, unsigned long long &key, int4 &rec) {
+  const int nb_total = st.nb_off[st.n_seq];
+  const int r = id / G, kk = id % G;
+  const int s = seq_of_row(st, r);
+  const int I = r - st.nb_off[s];
+  const int h = g * G + kk;
+  const int32_t *list = kb_idx + (int64_t)h * tri_total + st.tri_off[s] + (int64_t)I * (I + 1) / 2;
+  const int c_raw = kb_cnt[(int64_t)h * nb_total + r];
+  int32_t l[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) l[t] = list[min(t, I)];
+  const int cnt = max(0, min(c_raw, I + 1));
+  unsigned long long e[3];
+#pragma unroll
+  for (int t = 0; t < 3; ++t) e[t] = cnt > t + 1 ? min((unsigned)l[t + 1], 0x1FFFu) : 0x1FFFu;
+  const unsigned long long bucket = (unsigned long long)min(cnt >> 1, 1023);
+  key = ((1023ull - bucket) << 53) | (e[0] << 40) | (e[1] << 27) | (e[2] << 14) |
+        (unsigned long long)id;
+  rec = make_int4((int)(((uint32_t)s << 26) | ((uint32_t)kk << 13) | (uint32_t)I), cnt,
+                  cnt > 0 ? l[0] : -1, cnt > 1 ? l[1] : -1);
+}
+
+// Groups of more than kSortInline items have their keys and records built by item_keys
+// (one thread per item, before the sort) instead of by the sorting workgroup itself.
+constexpr int kSortInline = 4096;
+
+// Keys and records of every item of groups larger than kSortInline: keys[g][id],
+// recs[g][id].  Grid: (G * NB / 256, Hkv), 256 threads.
+__global__ __launch_bounds__(256) void item_keys(SeqTable st, const int32_t *kb_idx,
+                                                 const int32_t *kb_cnt, int hq, int hkv,
+                                                 int64_t tri_total, unsigned long long *keys,
+                                                 int4 *recs) {
+  const int G = hq / hkv;
+  const int n_g = G * st.nb_off[st.n_seq];
+  const int g = blockIdx.y;
+  const int id = blockIdx.x * blockDim.x + threadIdx.x;
+  if (id >= n_g) return;
+  unsigned long long key;
+  int4 rec;
+  item_key(st, kb_idx, kb_cnt, G, tri_total, g, id, key, rec);
+  keys[(int64_t)g * n_g + id] = key;
+  recs[(int64_t)g * n_g + id] = rec;
+}
+
+// One KV group's items in the order of their keys: the keys sorted in LDS, then each
+// item's record copied to its place.  Groups of up to kSortInline items build their keys
+// here (the records kept in LDS after the key slots), larger ones read those item_keys
+// wrote.  Also resets the queue counters.
 __device__ __forceinline__ void sort_group_items(const SeqTable &st, const int32_t *kb_idx,
                                                  const int32_t *kb_cnt, int hq, int hkv,
-                                                 int64_t tri_total, int4 *items, int32_t *queue,
+                                                 int64_t tri_total,
+                                                 const unsigned long long *keys,
+                                                 const int4 *recs, int4 *items, int32_t *queue,
                                                  int g, unsigned long long *key) {
   const int G = hq / hkv;
-  const int nb_total = st.nb_off[st.n_seq];
-  const int n_g = G * nb_total;
+  const int n_g = G * st.nb_off[st.n_seq];
   if (g == 0 && threadIdx.x < 8) queue[threadIdx.x] = 0;
   // sort slots: a power of two, at least one per thread
   int np = kSortThreads;
   while (np < n_g) np <<= 1;
-  // each item's record is kept in LDS after the keys when both fit (it is read back by id
-  // after the sort instead of being fetched again); the list entries are read together,
-  // at indices clamped to the row's capacity I + 1
-  const int rec0 = np;                          // records start 16-byte aligned
-  const bool stash = (size_t)rec0 * 8 + (size_t)n_g * 16 <= (size_t)kSortItems * 8;
-  int4 *rec = reinterpret_cast<int4 *>(key + rec0);
-  for (int id = threadIdx.x; id < np; id += blockDim.x) {
-    unsigned long long kv = ~0ull;               // padding sorts last
-    if (id < n_g) {
-      const int r = id / G, kk = id % G;
-      const int s = seq_of_row(st, r);
-      const int I = r - st.nb_off[s];
-      const int h = g * G + kk;
-      const int32_t *list = kb_idx + (int64_t)h * tri_total + st.tri_off[s] + (int64_t)I * (I + 1) / 2;
-      const int c_raw = kb_cnt[(int64_t)h * nb_total + r];
-      int32_t l[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) l[t] = list[min(t, I)];
-      const int cnt = max(0, min(c_raw, I + 1));
-      unsigned long long e[3];
-#pragma unroll
-      for (int t = 0; t < 3; ++t) e[t] = cnt > t + 1 ? min((unsigned)l[t + 1], 0x1FFFu) : 0x1FFFu;
-      const unsigned long long bucket = (unsigned long long)min(cnt >> 1, 1023);
-      kv = ((1023ull - bucket) << 53) | (e[0] << 40) | (e[1] << 27) | (e[2] << 14) |
-           (unsigned long long)id;
-      if (stash)
-        rec[id] = make_int4((int)(((uint32_t)s << 26) | ((uint32_t)kk << 13) | (uint32_t)I), cnt,
-                            cnt > 0 ? l[0] : -1, cnt > 1 ? l[1] : -1);
-    }
-    key[id] = kv;
+  const unsigned long long *src = keys + (int64_t)g * n_g;
+  const int4 *rsrc = recs + (int64_t)g * n_g;
+  if (n_g <= kSortInline) {
+    static_assert(kSortInline * (8 + 16) <= kSortItems * 8, "keys and records exceed the LDS");
+    int4 *rec = reinterpret_cast<int4 *>(key + np);
+    for (int id = threadIdx.x; id < n_g; id += blockDim.x)
+      item_key(st, kb_idx, kb_cnt, G, tri_total, g, id, key[id], rec[id]);
+    __syncthreads();
+    src = key;
+    rsrc = rec;
   }
-  __syncthreads();
   // bitonic sort, ascending, np / kSortThreads keys per thread held in registers
   switch (np / kSortThreads) {
-    case 1: sort_slots<1>(key); break;
-    case 2: sort_slots<2>(key); break;
-    case 4: sort_slots<4>(key); break;
-    case 8: sort_slots<8>(key); break;
-    default: sort_slots<16>(key); break;
+    case 1: sort_keys<1>(key, src, n_g); break;
+    case 2: sort_keys<2>(key, src, n_g); break;
+    case 4: sort_keys<4>(key, src, n_g); break;
+    case 8: sort_keys<8>(key, src, n_g); break;
+    default: sort_keys<16>(key, src, n_g); break;
   }
-  for (int t = threadIdx.x; t < n_g; t += blockDim.x) {
-    const int id = (int)(key[t] & 0x3FFF);
-    if (stash) {
-      items[(int64_t)g * n_g + t] = rec[id];
-    } else {
-      const int r = id / G, kk = id % G;
-      const int s = seq_of_row(st, r);
-      items[(int64_t)g * n_g + t] =
-          item_record(st, kb_idx, kb_cnt, nb_total, tri_total, G, g, s, kk, r - st.nb_off[s]);
-    }
-  }
+  for (int t = threadIdx.x; t < n_g; t += blockDim.x)
+    items[(int64_t)g * n_g + t] = rsrc[(int)(key[t] & 0x3FFF)];
 }
 
 
@@ -904,13 +928,16 @@ __device__ __forceinline__ void sort_group_items(const SeqTable &st, const int32
 template <int D, int B>
 __global__ __launch_bounds__(1024) void prepare_attn(SeqTable st, const int32_t *kb_idx,
                                                      const int32_t *kb_cnt, int hq, int hkv,
-                                                     int64_t tri_total, int4 *items,
+                                                     int64_t tri_total,
+                                                     const unsigned long long *keys,
+                                                     const int4 *recs, int4 *items,
                                                      int32_t *queue, const uint16_t *v,
                                                      int nb_total, uint16_t *vt) {
   static_assert(4 * B * D * 2 <= kSortItems * 8, "V^T tiles exceed the shared LDS");
   __shared__ __attribute__((aligned(16))) unsigned long long smem[kSortItems];
   if ((int)blockIdx.x < hkv) {
-    sort_group_items(st, kb_idx, kb_cnt, hq, hkv, tri_total, items, queue, blockIdx.x, smem);
+    sort_group_items(st, kb_idx, kb_cnt, hq, hkv, tri_total, keys, recs, items, queue,
+                     blockIdx.x, smem);
     return;
   }
   const int q = threadIdx.x >> 8;
@@ -929,10 +956,14 @@ hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t stream) {
   auto prepare = [&](auto dc, auto bc) {
     constexpr int D = decltype(dc)::value, B = decltype(bc)::value;
     if (n_g <= kSortItems) {
+      if (n_g > kSortInline)
+        hipLaunchKernelGGL(item_keys, dim3((int)((n_g + 255) / 256), a.hkv), dim3(256), 0,
+                           stream, a.st, a.kb_idx, a.kb_cnt, a.hq, a.hkv, a.tri_total,
+                           a.sort_keys, a.sort_recs);
       const int tiles = a.nb_total * a.hkv;
       hipLaunchKernelGGL((prepare_attn<D, B>), dim3(a.hkv + (tiles + 3) / 4), dim3(1024), 0,
-                         stream, a.st, a.kb_idx, a.kb_cnt, a.hq, a.hkv, a.tri_total, a.items,
-                         a.queue, a.v, a.nb_total, a.vt);
+                         stream, a.st, a.kb_idx, a.kb_cnt, a.hq, a.hkv, a.tri_total,
+                         a.sort_keys, a.sort_recs, a.items, a.queue, a.v, a.nb_total, a.vt);
     } else {
       hipLaunchKernelGGL(build_item_order_plain, dim3((a.nb_total + 255) / 256), dim3(256), 0,
                          stream, a.st, a.kb_idx, a.kb_cnt, a.hq, a.hkv, a.tri_total, a.items,

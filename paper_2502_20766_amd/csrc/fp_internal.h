@@ -100,6 +100,8 @@ struct AttnArgs {
   int32_t *queue;          // [8] workspace: per-XCD work-queue counters
   int32_t mix;             // set by the launcher: an XCD's KV groups served interleaved
   uint16_t *vt;            // [Hkv][NB][B * d] workspace: V^T tiles per key block
+  unsigned long long *sort_keys;  // [Hkv][G * NB] workspace: items' sort keys
+  int4 *sort_recs;         // [Hkv][G * NB] workspace: item records in item-id order
 };
 
 // Device address of the current device's fixed scratch array (fp_noalloc.hip).
