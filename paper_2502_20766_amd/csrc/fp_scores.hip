@@ -13,8 +13,9 @@
 // shape.  Each pass-2 workgroup owns the slash offsets whose last-row key falls in its
 // chunk and recomputes the 128 keys before the chunk so that it sees those diagonals whole.
 //
-// Block pooling (avgpool with window block_size, aligned at token 0 of each sequence) is
-// a separate streaming kernel used for K (all KV heads) and Q (query-aware heads only).
+// Block pooling (avgpool with window block_size, aligned at token 0 of each sequence): K̄
+// (every KV head) is summed by pass 1 from the K tiles it streams anyway, Q̄ (query-aware
+// heads only) by a separate streaming kernel.
 #include <type_traits>
 
 #include "fp_internal.h"
@@ -58,6 +59,7 @@ struct KTile {
   static constexpr int NIT = CH >= NT ? CH / NT : 1;    // chunks per thread (threads past
                                                         // CH stay idle)
   static_assert(CH < NT || NIT * NT == CH, "tile chunks must divide over the threads");
+  static_assert(KCH == 8 || KCH == 16, "head dim 64 or 128");
   uint4 v[NIT];
   __device__ __forceinline__ void load(const uint16_t *kbase, int64_t kv_row, int kt, int n,
                                        int tid) {
@@ -129,11 +131,18 @@ __device__ __forceinline__ void load_qhat(const SelectArgs &a, int tok0, int n, 
 
 // HG query heads of one KV group per workgroup (4 waves each), sharing every K tile: the
 // chunk's K is read once for HG heads (HG = 4 fits in 128 registers per lane, so the
-// 16 waves of a workgroup are resident together).
+// 16 waves of a workgroup are resident together).  The workgroup holding the first heads
+// of its KV group also writes K̄ for the chunk's key blocks: each thread adds up its
+// 16-byte pieces of the block's tiles (all in one column of 8 dimensions), the lanes of a
+// wave holding one column are summed by a fixed xor tree, and the waves' partial sums in
+// order through LDS.
 template <int D, int HG>
 __global__ __launch_bounds__(kThreads * HG) void rep_stats(SelectArgs a) {
   constexpr int NT = kThreads * HG;
+  using Tile = KTile<D, NT>;
+  constexpr int NSLOT = (Tile::CH < NT ? Tile::CH : NT) / 64;   // waves holding tile pieces
   __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * D];
+  __shared__ float kpart[NSLOT][D];          // per wave: sums over its keys of the block
   const int c = blockIdx.x;
   const int h = blockIdx.y * HG + (threadIdx.x >> 8);
   const int s = seq_of_chunk(a.st, c);
@@ -153,12 +162,61 @@ __global__ __launch_bounds__(kThreads * HG) void rep_stats(SelectArgs a) {
   bf16x8 qf[D / 16];
   load_qhat<D>(a, tok0, n, h, r, lh, qf);
   float m = -INFINITY, l = 0.f;
-  KTile<D, NT> tile;
+  // K̄ of this chunk's blocks: by the workgroup of the KV group's first heads
+  const bool pool = (blockIdx.y * HG) % G == 0;
+  // thread tid's pieces of a tile are chunks it * NT + tid: keys (it * NT + tid) / KCH, all
+  // in column tid % KCH (NT is a multiple of KCH)
+  float ksum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  Tile tile;
   tile.load(kbase, kv_row, c0, n, tid);
   for (int kt = c0; kt < c1; kt += KT) {
     __syncthreads();
+    // the tile ends a key block (tiles never straddle one: chunks start on a block
+    // boundary and KT divides the block)
+    const bool block_end = (kt + KT) % a.block == 0 || kt + KT >= c1;
+    if (pool) {
+#pragma unroll
+      for (int it = 0; it < Tile::NIT; ++it) {
+        if (Tile::CH < NT && tid >= Tile::CH) continue;     // idle in the tile copy
+        const uint32_t wv[4] = {tile.v[it].x, tile.v[it].y, tile.v[it].z, tile.v[it].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          ksum[2 * i] += __uint_as_float(wv[i] << 16);
+          ksum[2 * i + 1] += __uint_as_float(wv[i] & 0xFFFF0000u);
+        }
+      }
+      if (block_end) {
+        // the lanes of a wave with one column differ in the lane bits from KCH up: pairs
+        // 16 and 32 apart are added by the row and half swaps (lower lane first), 8 apart
+        // by a lane shuffle
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          if constexpr (Tile::KCH <= 8) ksum[e] += __shfl_xor(ksum[e], 8);
+          const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(ksum[e]),
+                                                            __float_as_uint(ksum[e]), false, false);
+          ksum[e] = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+          const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(ksum[e]),
+                                                            __float_as_uint(ksum[e]), false, false);
+          ksum[e] = __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
+        }
+        if (tid < Tile::CH && lane < Tile::KCH) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) kpart[tid / 64][lane * 8 + e] = ksum[e];
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ksum[e] = 0.f;
+      }
+    }
     tile.store(Ks, tid);
     __syncthreads();
+    if (pool && block_end && tid < D) {
+      float sum = 0.f;
+#pragma unroll
+      for (int q = 0; q < NSLOT; ++q) sum += kpart[q][tid];
+      const int J = kt / a.block;
+      const int cntk = min(a.block, n - J * a.block);
+      a.kbar[((int64_t)(a.st.nb_off[s] + J) * a.hkv + h / G) * D + tid] = sum / (float)cntk;
+    }
     if (kt + KT < c1) tile.load(kbase, kv_row, kt + KT, n, tid);   // overlaps this tile
     f32x16 sacc[2];
     tile_scores<D>(Ks, qf, lr, lh, sacc);
@@ -435,15 +493,8 @@ hipError_t launch_rep_scores(const SelectArgs &a, hipStream_t stream) {
   }
   hipLaunchKernelGGL(rep_stats_combine, dim3(a.st.n_seq, a.hq, (a.block + 3) / 4), dim3(256), 0,
                      stream, a);
-  if (a.d == 128) {
-    hipLaunchKernelGGL(rep_lines<128>, grid, dim3(kThreads), 0, stream, a);
-    hipLaunchKernelGGL(pool_blocks<128>, dim3(a.nb_total, a.hkv), dim3(kThreads), 0, stream, a.st,
-                       a.k, a.hkv, a.block, a.kbar, (const uint8_t *)nullptr, a.hq, 0);
-  } else {
-    hipLaunchKernelGGL(rep_lines<64>, grid, dim3(kThreads), 0, stream, a);
-    hipLaunchKernelGGL(pool_blocks<64>, dim3(a.nb_total, a.hkv), dim3(kThreads), 0, stream, a.st,
-                       a.k, a.hkv, a.block, a.kbar, (const uint8_t *)nullptr, a.hq, 0);
-  }
+  if (a.d == 128) hipLaunchKernelGGL(rep_lines<128>, grid, dim3(kThreads), 0, stream, a);
+  else hipLaunchKernelGGL(rep_lines<64>, grid, dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
