@@ -725,32 +725,44 @@ __device__ __forceinline__ int seq_of_row(const SeqTable &st, int r) {
 // V^T tiles for the attention stages: for KV head h and global key block gb (B keys of
 // one sequence), the B x D slice of V is written as B/16 steps of [d][16 keys], each
 // 16-byte unit (8 keys of one d) at vt_unit(d, key half) of its step -- the order the
-// attention kernel keeps in LDS.  Keys past the sequence end are zero.  One tile per call,
-// by the nt threads tid = 0 .. nt-1 of the caller, all of which reach the barrier inside
-// (valid = false: no tile, barrier only).  `tile` is B * D * 2 bytes of LDS.
+// attention kernel keeps in LDS.  Keys past the sequence end are zero.  A tile goes
+// through 256 threads: load() takes its rows of V into registers, to_lds() stores them in
+// a [key][d] LDS tile (`tile`, B * D * 2 bytes; unit index XOR key % (D / 8)), and after a
+// barrier store_vt() writes the transposed tile.
 template <int D, int B>
-__device__ __forceinline__ void transpose_v_tile(const SeqTable &st, const uint16_t *v, int hkv,
-                                                 int nb_total, uint16_t *vt, int gb, int h,
-                                                 bool valid, uint4 *tile, int tid, int nt) {
-  constexpr int UPR = D / 8;               // 16-byte units per key row of the slice
-  int tok = 0, nvalid = 0;
-  if (valid) {
+struct VtTile {
+  static constexpr int UPR = D / 8;              // 16-byte units per key row of the slice
+  static constexpr int PER = B * UPR / 256;      // units per thread
+  uint4 val[PER];
+  __device__ __forceinline__ void load(const SeqTable &st, const uint16_t *v, int hkv, int gb,
+                                       int h, int tid) {
     const int s = seq_of_row(st, gb);
-    tok = st.cu[s] + (gb - st.nb_off[s]) * B;
-    nvalid = min(B, st.cu[s + 1] - tok);
-    for (int u = tid; u < B * UPR; u += nt) {  // [key][d], unit index XOR (key % UPR)
-      const int key = u / UPR, c = u % UPR;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (key < nvalid)
-        val = *reinterpret_cast<const uint4 *>(v + ((int64_t)(tok + key) * hkv + h) * D + 8 * c);
-      tile[key * UPR + (c ^ (key % UPR))] = val;
+    const int tok = st.cu[s] + (gb - st.nb_off[s]) * B;
+    const int nvalid = min(B, st.cu[s + 1] - tok);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int u = tid + 256 * i, key = u / UPR, c = u % UPR;
+      val[i] = key < nvalid
+                   ? *reinterpret_cast<const uint4 *>(v + ((int64_t)(tok + key) * hkv + h) * D + 8 * c)
+                   : make_uint4(0, 0, 0, 0);
     }
   }
-  __syncthreads();
-  if (!valid) return;
+  __device__ __forceinline__ void to_lds(uint4 *tile, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int u = tid + 256 * i, key = u / UPR, c = u % UPR;
+      tile[key * UPR + (c ^ (key % UPR))] = val[i];
+    }
+  }
+};
+
+template <int D, int B>
+__device__ __forceinline__ void store_vt(const uint4 *tile, uint16_t *vt, int nb_total, int gb,
+                                         int h, int tid) {
+  constexpr int UPR = D / 8;
   const uint16_t *t16 = reinterpret_cast<const uint16_t *>(tile);
   uint4 *out = reinterpret_cast<uint4 *>(vt + ((int64_t)h * nb_total + gb) * B * D);
-  for (int p = tid; p < B * UPR; p += nt) {
+  for (int p = tid; p < B * UPR; p += 256) {
     const int step = p / (2 * D), w = p % (2 * D);
     const int d = 8 * (w >> 4) + (w & 7);
     const int lh = ((w >> 3) & 1) ^ ((w >> 4) & 1);
@@ -771,8 +783,11 @@ template <int D, int B>
 __global__ __launch_bounds__(256) void stage_v_transposed(SeqTable st, const uint16_t *v, int hkv,
                                                           int nb_total, uint16_t *vt) {
   __shared__ uint4 tile[B * D / 8];
-  transpose_v_tile<D, B>(st, v, hkv, nb_total, vt, blockIdx.x, blockIdx.y, true, tile,
-                         threadIdx.x, blockDim.x);
+  VtTile<D, B> t;
+  t.load(st, v, hkv, blockIdx.x, blockIdx.y, threadIdx.x);
+  t.to_lds(tile, threadIdx.x);
+  __syncthreads();
+  store_vt<D, B>(tile, vt, nb_total, blockIdx.x, blockIdx.y, threadIdx.x);
 }
 
 // Plain item order, used when a group has too many items for the in-LDS sort: rows by query
@@ -923,8 +938,9 @@ __device__ __forceinline__ void sort_group_items(const SeqTable &st, const int32
 
 
 // One launch for both preparations of the attention: workgroups 0 .. Hkv-1 sort their KV
-// group's items (as above), the others write the V^T tiles, four per workgroup (one per 256
-// threads), on the CUs the sort leaves idle.  1024 threads; 128 KB of LDS shared by both.
+// group's items (as above), the others (about one per CU the sort leaves) write the V^T
+// tiles, four at a time per workgroup (one per 256 threads).  1024 threads; 128 KB of LDS
+// shared by both.
 template <int D, int B>
 __global__ __launch_bounds__(1024) void prepare_attn(SeqTable st, const int32_t *kb_idx,
                                                      const int32_t *kb_cnt, int hq, int hkv,
@@ -940,18 +956,38 @@ __global__ __launch_bounds__(1024) void prepare_attn(SeqTable st, const int32_t 
                      blockIdx.x, smem);
     return;
   }
-  const int q = threadIdx.x >> 8;
-  const int t = (blockIdx.x - hkv) * 4 + q;            // tile = gb * Hkv + h
-  const bool valid = t < nb_total * hkv;
+  // V^T workgroups: tiles t = gb * Hkv + h, four at a time (one per 256 threads); each
+  // workgroup takes every step-th group of four, loading the next group's rows while it
+  // writes the current group's transposed tiles
+  const int q = threadIdx.x >> 8, tid = threadIdx.x & 255;
   uint4 *tile = reinterpret_cast<uint4 *>(smem) + q * (B * D / 8);
-  transpose_v_tile<D, B>(st, v, hkv, nb_total, vt, valid ? t / hkv : 0, valid ? t % hkv : 0,
-                         valid, tile, threadIdx.x & 255, 256);
+  const int ntiles = nb_total * hkv;
+  const int step = ((int)gridDim.x - hkv) * 4;
+  const int first = ((int)blockIdx.x - hkv) * 4;
+  VtTile<D, B> cur;
+  if (first + q < ntiles) cur.load(st, v, hkv, (first + q) / hkv, (first + q) % hkv, tid);
+  for (int base = first; base < ntiles; base += step) {
+    const int tc = base + q, tn = tc + step;
+    if (tc < ntiles) cur.to_lds(tile, tid);
+    __syncthreads();
+    if (tn < ntiles) cur.load(st, v, hkv, tn / hkv, tn % hkv, tid);
+    if (tc < ntiles) store_vt<D, B>(tile, vt, nb_total, tc / hkv, tc % hkv, tid);
+    __syncthreads();
+  }
 }
 }  // namespace
 
 hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t stream) {
   const int G = a.hq / a.hkv;
   const int64_t n_g = (int64_t)G * a.nb_total;
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      cus = 256;
+  }
   // item order and V^T tiles: one fused launch when the groups fit the in-LDS sort
   auto prepare = [&](auto dc, auto bc) {
     constexpr int D = decltype(dc)::value, B = decltype(bc)::value;
@@ -960,8 +996,11 @@ hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t stream) {
         hipLaunchKernelGGL(item_keys, dim3((int)((n_g + 255) / 256), a.hkv), dim3(256), 0,
                            stream, a.st, a.kb_idx, a.kb_cnt, a.hq, a.hkv, a.tri_total,
                            a.sort_keys, a.sort_recs);
-      const int tiles = a.nb_total * a.hkv;
-      hipLaunchKernelGGL((prepare_attn<D, B>), dim3(a.hkv + (tiles + 3) / 4), dim3(1024), 0,
+      // V^T workgroups: one per CU left by the sorting ones (each holds all of a CU's LDS
+      // it may use), no more than there are groups of four tiles
+      const int groups = (a.nb_total * a.hkv + 3) / 4;
+      const int vt_wgs = std::max(1, std::min(cus - a.hkv, groups));
+      hipLaunchKernelGGL((prepare_attn<D, B>), dim3(a.hkv + vt_wgs), dim3(1024), 0,
                          stream, a.st, a.kb_idx, a.kb_cnt, a.hq, a.hkv, a.tri_total,
                          a.sort_keys, a.sort_recs, a.items, a.queue, a.v, a.nb_total, a.vt);
     } else {
@@ -983,14 +1022,6 @@ hipError_t launch_sparse_attn(const AttnArgs &a, hipStream_t stream) {
   }
   // Persistent grid: resident workgroups for two waves per SIMD (a multiple of 8, one
   // share per XCD), no more than there are items.
-  static int cus = 0;
-  if (cus == 0) {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        cus <= 0)
-      cus = 256;
-  }
   const int64_t total = n_g * a.hkv;
   auto grid = [&](int wg_per_cu) {
     return (int)std::min<int64_t>((wg_per_cu * cus / 8) * 8, (total + 7) / 8 * 8);
