@@ -8,7 +8,7 @@
 // One workgroup = one (sequence, query head, query block) row of B queries; B/32 waves of
 // 32 query rows each.  Per selected key block, in stages of B/2 keys:
 //   * K tile [keys][d] is staged in LDS row-major with a 16-byte-chunk XOR swizzle;
-//   * V is transposed once per call (transpose_v_tile, in the preparation launch) into
+//   * V is transposed once per call (VtTile / store_vt, in the preparation launch) into
 //     16-key steps of V^T, [step][d][16 keys], already in the swizzled LDS order, so its
 //     stage copy is linear and each V^T fragment is one conflict-free ds_read_b128;
 //   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (Q^T fragments live in registers), so each
