@@ -183,6 +183,13 @@ def test_sparse_attention_rising_and_jumping_scores(block):
 
 # ---------------------------------------------------------------- full path vs oracle
 
+# the largest packed batch the ABI takes (FP_MAX_BATCH = 64 sequences), lengths from 1 token
+# to ~2200 around block multiples
+MAX_BATCH_SEQLENS = (1, 2, 3, 64, 65, 127, 128, 129) + tuple(
+    (37 * i * i + 11 * i) % 2200 + 1 for i in range(56))
+MAX_BATCH = synth.SPECS["qwen_varlen"].with_seqlens(MAX_BATCH_SEQLENS, "max-batch-64").with_params(
+    hq=8, hkv=2, head_kinds=("vs", "qa") * 4)
+
 SELECT_CASES = [
     ("tiny", synth.SPECS["tiny"], None),
     ("mixed-8h-n8192", synth.SPECS["llama32k"].with_seqlens((8192,), "mixed-8h-n8192")
@@ -190,6 +197,7 @@ SELECT_CASES = [
     ("ragged-varlen", synth.SPECS["qwen_varlen"].with_seqlens((300, 129, 1, 2000, 4096),
                                                               "ragged-varlen"), None),
     ("glm-gqa16-n8192", synth.SPECS["glm64k"].with_seqlens((8192,), "glm-gqa16-n8192"), None),
+    ("max-batch-64", MAX_BATCH, None),
 ]
 
 
@@ -408,6 +416,7 @@ B64_SELECT_CASES = [
     ("b64-mixed-8h-n8192", MIXED.with_params(block=64)),
     ("b64-ragged-varlen", RAGGED.with_params(block=64)),
     ("b64-glm-gqa16-n8192", GLM.with_params(block=64)),
+    ("b64-max-batch-64", MAX_BATCH.with_params(block=64)),
 ]
 
 
