@@ -198,6 +198,10 @@ SELECT_CASES = [
                                                               "ragged-varlen"), None),
     ("glm-gqa16-n8192", synth.SPECS["glm64k"].with_seqlens((8192,), "glm-gqa16-n8192"), None),
     ("max-batch-64", MAX_BATCH, None),
+    # d 64 with four query heads per statistics workgroup (half of its threads take no part
+    # in the tile copy): 64 / 16 heads at 32k
+    ("d64-gqa4-n32768", synth.SPECS["llama32k"].with_params(
+        hq=64, hkv=16, d=64, head_kinds=("vs", "qa") * 32), None),
 ]
 
 
