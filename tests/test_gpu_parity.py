@@ -314,6 +314,10 @@ VARIANT_CASES = [
     ("pooled-mixed-8h-n8192", MIXED, 0, 0, None, 1),
     ("pooled-ragged-varlen", RAGGED, 0, 0, None, 1),
     ("pooled-rows-cap10-mixed-8h-n8192", MIXED, 1, 10, None, 1),
+    # the ends of the minimum budget's range: none, and FP_MAX_MIN_BUDGET blocks
+    ("min0-mixed-8h-n8192", MIXED, 0, 0, 0, 0),
+    ("min64-ragged-varlen", RAGGED, 0, 0, 64, 0),
+    ("rows-min64-glm-gqa16-n8192", GLM, 1, 0, 64, 0),
 ]
 
 
