@@ -5,13 +5,12 @@
 
 namespace fp {
 
-__device__ __forceinline__ unsigned long long key_min(unsigned long long u,
-                                                      unsigned long long v) {
-  return v < u ? v : u;
-}
-__device__ __forceinline__ unsigned long long key_max(unsigned long long u,
-                                                      unsigned long long v) {
-  return v < u ? u : v;
+// One side of a compare-exchange: the partner's key v if (v < u) == take_min, else the own
+// key u -- min(u, v) when take_min, max(u, v) otherwise (equal keys: either is the value).
+// One 64-bit compare and two selects per key.
+__device__ __forceinline__ unsigned long long key_keep(unsigned long long u,
+                                                       unsigned long long v, bool take_min) {
+  return ((v < u) == take_min) ? v : u;
 }
 
 // One compare-exchange stage (SIZE, STRIDE) of an ascending bitonic sort of NT*E keys,
@@ -28,7 +27,7 @@ __device__ __forceinline__ void bitonic_stage(unsigned long long (&k)[E],
         const int f = e | STRIDE;
         const bool up = ((tid * E + e) & SIZE) == 0;
         const unsigned long long u = k[e], v = k[f];
-        const bool sw = up ? (u > v) : (u < v);
+        const bool sw = (v < u) == up;     // out of order for this half (equal: no matter)
         k[e] = sw ? v : u;
         k[f] = sw ? u : v;
       }
@@ -39,7 +38,7 @@ __device__ __forceinline__ void bitonic_stage(unsigned long long (&k)[E],
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const unsigned long long v = __shfl_xor(k[e], LX);
-      k[e] = take_min ? key_min(k[e], v) : key_max(k[e], v);
+      k[e] = key_keep(k[e], v, take_min);
     }
   } else {
     // Position tid * E + e pairs with (tid ^ TX) * E + e.  The exchange is stored
@@ -55,7 +54,7 @@ __device__ __forceinline__ void bitonic_stage(unsigned long long (&k)[E],
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const unsigned long long v = lds[e * NT + (tid ^ TX)];
-      k[e] = take_min ? key_min(k[e], v) : key_max(k[e], v);
+      k[e] = key_keep(k[e], v, take_min);
     }
   }
   if constexpr (STRIDE > 1) bitonic_stage<NT, E, SIZE, STRIDE / 2>(k, lds, tid);
