@@ -19,8 +19,7 @@
 //     reference max moves (with the O rescale) only when a score rises more than 2^8 in
 //     weight terms above it, so most stages skip the rescale;
 //   * the two LDS stage buffers alternate within each key block (every row takes an even
-//     number of stages), so with block 128 the unrolled stage pair reads them at constant
-//     offsets;
+//     number of stages), so the unrolled stage pair reads them at constant offsets;
 //   * O^T += V^T P^T on the same MFMA, and O^T keeps one query row per lane, so the
 //     rescale by exp2(m_old - m_new) is per lane.
 // A persistent grid walks each KV group's (sequence, query head, query block) items in a
@@ -554,8 +553,7 @@ void sparse_fa_fwd(AttnArgs a) {
     // stage t covers keys J*B + (B/2)*(t&1) .. of block J = list[t >> 1]; a row with no
     // blocks still takes two (empty) stages so that its zero output is written.  Every row
     // has an even number of stages, so even stages read LDS buffer 0 and odd ones buffer 1;
-    // with 64-key stages the loop is unrolled by two, which makes each buffer's read
-    // offsets constants.
+    // the loop is unrolled by two, which makes each buffer's read offsets constants.
     const int n_stages = 2 * max(cur.cnt, 1);
     auto stage = [&](auto cbc, const int t) {
       const int CB = cbc;                        // LDS buffer of this stage's K/V tiles
@@ -669,15 +667,9 @@ void sparse_fa_fwd(AttnArgs a) {
         pv_step(std::integral_constant<int, 3>{}, pf[3]);
       }
     };
-    if constexpr (B == 128) {
-      for (int t = 0; t < n_stages; t += 2) {
-        stage(std::integral_constant<int, 0>{}, t);
-        stage(std::integral_constant<int, 1>{}, t + 1);
-      }
-    } else {
-      // 32-key stages: one stage body, its buffer taken from the stage's parity (the
-      // unrolled pair measured 10% slower over every causal block at this size)
-      for (int t = 0; t < n_stages; ++t) stage(t & 1, t);
+    for (int t = 0; t < n_stages; t += 2) {
+      stage(std::integral_constant<int, 0>{}, t);
+      stage(std::integral_constant<int, 1>{}, t + 1);
     }
 
     // ---- normalise and store: lane holds query row qrow, d = 32db + 8(v/4) + 4lh + v%4
