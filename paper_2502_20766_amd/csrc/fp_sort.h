@@ -13,6 +13,22 @@ __device__ __forceinline__ unsigned long long key_keep(unsigned long long u,
   return ((v < u) == take_min) ? v : u;
 }
 
+// The value of lane l ^ LX (LX < 64): DPP moves inside quads and rows, a swizzle inside
+// 32-lane groups, a permute across the halves.
+template <int LX>
+__device__ __forceinline__ unsigned lane_xor32(unsigned x) {
+  if constexpr (LX == 1) return (unsigned)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, false);
+  else if constexpr (LX == 2) return (unsigned)__builtin_amdgcn_mov_dpp((int)x, 0x4E, 0xF, 0xF, false);
+  else if constexpr (LX == 8) return (unsigned)__builtin_amdgcn_mov_dpp((int)x, 0x128, 0xF, 0xF, false);
+  else if constexpr (LX == 4 || LX == 16) return (unsigned)__builtin_amdgcn_ds_swizzle((int)x, 0x1F | (LX << 10));
+  else return (unsigned)__shfl_xor((int)x, LX);
+}
+template <int LX>
+__device__ __forceinline__ unsigned long long lane_xor(unsigned long long x) {
+  const unsigned lo = lane_xor32<LX>((unsigned)x), hi = lane_xor32<LX>((unsigned)(x >> 32));
+  return ((unsigned long long)hi << 32) | lo;
+}
+
 // One compare-exchange stage (SIZE, STRIDE) of an ascending bitonic sort of NT*E keys,
 // thread t holding positions t*E .. t*E+E-1 in k[].  Strides below E pair keys of one
 // thread, strides below 64*E pair lanes of one wave, wider strides go through `lds`
@@ -37,7 +53,7 @@ __device__ __forceinline__ void bitonic_stage(unsigned long long (&k)[E],
     const bool take_min = ((tid & LX) == 0) == (((tid * E) & SIZE) == 0);
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      const unsigned long long v = __shfl_xor(k[e], LX);
+      const unsigned long long v = lane_xor<LX>(k[e]);
       k[e] = key_keep(k[e], v, take_min);
     }
   } else {
