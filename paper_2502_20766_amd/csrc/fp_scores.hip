@@ -129,29 +129,30 @@ __device__ __forceinline__ void load_qhat(const SelectArgs &a, int tok0, int n, 
 
 // ---------------------------------------------------------------- pass 1: row max / sum
 
-// HG query heads of one KV group per workgroup (4 waves each), sharing every K tile: the
-// chunk's K is read once for HG heads (HG = 4 fits in 128 registers per lane, so the
-// 16 waves of a workgroup are resident together).  The workgroup holding the first heads
+// HG query heads of one KV group per workgroup, RW waves of 32 representative rows each
+// (4 at block 128, 2 at block 64), sharing every K tile: the chunk's K is read once for HG
+// heads (HG = 4 fits in 128 registers per lane, so the 16 waves of a block-128 workgroup
+// are resident together).  The workgroup holding the first heads
 // of its KV group also writes K̄ for the chunk's key blocks: each thread adds up its
 // 16-byte pieces of the block's tiles (all in one column of 8 dimensions), the lanes of a
 // wave holding one column are summed by a fixed xor tree, and the waves' partial sums in
 // order through LDS.
-template <int D, int HG>
-__global__ __launch_bounds__(kThreads * HG) void rep_stats(SelectArgs a) {
-  constexpr int NT = kThreads * HG;
+template <int D, int HG, int RW>
+__global__ __launch_bounds__(64 * RW * HG) void rep_stats(SelectArgs a) {
+  constexpr int NT = 64 * RW * HG;
   using Tile = KTile<D, NT>;
   constexpr int NSLOT = (Tile::CH < NT ? Tile::CH : NT) / 64;   // waves holding tile pieces
   __shared__ __attribute__((aligned(16))) uint16_t Ks[KT * D];
   __shared__ float kpart[NSLOT][D];          // per wave: sums over its keys of the block
   const int c = blockIdx.x;
-  const int h = blockIdx.y * HG + (threadIdx.x >> 8);
+  const int h = blockIdx.y * HG + (int)threadIdx.x / (64 * RW);
   const int s = seq_of_chunk(a.st, c);
   const int tok0 = a.st.cu[s];
   const int n = a.st.cu[s + 1] - tok0;
   const int bp = min(a.block, n);
   const int c0 = (c - a.st.ch_off[s]) * a.st.ch_len;
   const int c1 = min(c0 + a.st.ch_len, n);
-  const int tid = threadIdx.x, w = (tid >> 6) & 3, lane = tid & 63, lr = lane & 31, lh = lane >> 5;
+  const int tid = threadIdx.x, w = (tid >> 6) % RW, lane = tid & 63, lr = lane & 31, lh = lane >> 5;
   const int r = 32 * w + lr;                 // representative row of this lane
   const int irow = n - bp + r;               // its absolute position i_r
   const int G = a.hq / a.hkv;
@@ -260,7 +261,7 @@ __global__ __launch_bounds__(kThreads * HG) void rep_stats(SelectArgs a) {
   const float mu = (mm == -INFINITY) ? 0.f : mm;
   // fixed order: lower half's partial first
   const float lt = la * __builtin_amdgcn_exp2f(ma - mu) + lb * __builtin_amdgcn_exp2f(mb - mu);
-  // rows r >= block do not exist (block 64 uses two of the four waves' rows)
+  // rows r >= block do not exist (the RW waves cover exactly the block's rows; kept as a guard)
   if (lh == 0 && r < a.block)
     a.chunk_stats[((int64_t)c * a.hq + h) * a.block + r] = make_float2(mm, lt);
 }
@@ -481,15 +482,25 @@ hipError_t launch_rep_scores(const SelectArgs &a, hipStream_t stream) {
   int hg = G % 4 == 0 ? 4 : (G % 2 == 0 ? 2 : 1);
   // short problems: fewer heads per workgroup, so that the grid still covers the GPU
   while (hg > 1 && (int64_t)ch_total * (a.hq / hg) < 512) hg /= 2;
-  const dim3 grid_g(ch_total, a.hq / hg), block_g(kThreads * hg);
+  // one wave per 32 representative rows: 4 per head at block 128, 2 at block 64
+  const int rw = a.block == 64 ? 2 : 4;
+  const dim3 grid_g(ch_total, a.hq / hg), block_g(64 * rw * hg);
+  auto stats = [&](auto dc, auto rwc) {
+    constexpr int D = decltype(dc)::value, RW = decltype(rwc)::value;
+    if (hg == 4) hipLaunchKernelGGL((rep_stats<D, 4, RW>), grid_g, block_g, 0, stream, a);
+    else if (hg == 2) hipLaunchKernelGGL((rep_stats<D, 2, RW>), grid_g, block_g, 0, stream, a);
+    else hipLaunchKernelGGL((rep_stats<D, 1, RW>), grid_g, block_g, 0, stream, a);
+  };
+  using I128 = std::integral_constant<int, 128>;
+  using I64 = std::integral_constant<int, 64>;
+  using I4 = std::integral_constant<int, 4>;
+  using I2 = std::integral_constant<int, 2>;
   if (a.d == 128) {
-    if (hg == 4) hipLaunchKernelGGL((rep_stats<128, 4>), grid_g, block_g, 0, stream, a);
-    else if (hg == 2) hipLaunchKernelGGL((rep_stats<128, 2>), grid_g, block_g, 0, stream, a);
-    else hipLaunchKernelGGL((rep_stats<128, 1>), grid_g, block_g, 0, stream, a);
+    if (rw == 4) stats(I128{}, I4{});
+    else stats(I128{}, I2{});
   } else {
-    if (hg == 4) hipLaunchKernelGGL((rep_stats<64, 4>), grid_g, block_g, 0, stream, a);
-    else if (hg == 2) hipLaunchKernelGGL((rep_stats<64, 2>), grid_g, block_g, 0, stream, a);
-    else hipLaunchKernelGGL((rep_stats<64, 1>), grid_g, block_g, 0, stream, a);
+    if (rw == 4) stats(I64{}, I4{});
+    else stats(I64{}, I2{});
   }
   hipLaunchKernelGGL(rep_stats_combine, dim3(a.st.n_seq, a.hq, (a.block + 3) / 4), dim3(256), 0,
                      stream, a);
