@@ -293,25 +293,28 @@ __global__ __launch_bounds__(256) void rep_stats_combine(SelectArgs a) {
 
 // ---------------------------------------------------------------- pass 2: line sums
 
-// 32-key tiles: each wave computes S = Q_hat K^T for its 32 rows and the tile's 32 keys
-// with one MFMA block, so a lane holds one key and 16 rows and the column sums (vertical
-// lines) are in-lane adds plus one half-wave swap.  The weights go to an LDS tile whose
-// diagonals (slash lines) are summed by the workgroup.  The small tile keeps the LDS and
-// register footprint low enough for four workgroups per CU, which hides the latency of
-// the barrier-separated phases.
+// 32-key tiles: each of the RW waves (one per 32 representative rows: 4 at block 128, 2 at
+// block 64) computes S = Q_hat K^T for its 32 rows and the tile's 32 keys with one MFMA
+// block, so a lane holds one key and 16 rows and the column sums (vertical lines) are
+// in-lane adds plus one half-wave swap.  The weights go to an LDS tile whose diagonals
+// (slash lines) are summed by the workgroup.  The small tile keeps the LDS and register
+// footprint low enough for several workgroups per CU, which hides the latency of the
+// barrier-separated phases.
 constexpr int LKT = 32;                        // keys per line-pass tile
 constexpr int LPITCH = LKT + 1;                // odd pitch: diagonal reads are conflict free
 constexpr int LPAD = LKT - 1;                  // zero rows above and below the weight rows
 
-template <int D>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void rep_lines(
+template <int D, int RW>
+__global__ __launch_bounds__(64 * RW) __attribute__((amdgpu_waves_per_eu(RW))) void rep_lines(
     SelectArgs a) {
+  constexpr int NT = 64 * RW;                  // threads: one wave per 32 representative rows
+  constexpr int ROWS = 32 * RW;                // rows of the weight tile (the block size)
   __shared__ __attribute__((aligned(16))) uint16_t Ks[LKT * D];   // K tile
   // Â tile, [row][key], with LPAD zero rows on both sides: every diagonal of the tile is
   // then LKT reads at fixed offsets (the rows past b' hold zero weights)
-  __shared__ float Pt[(LPAD + 128 + LPAD) * LPITCH];
+  __shared__ float Pt[(LPAD + ROWS + LPAD) * LPITCH];
   __shared__ float acc_s[kScoreChunk];         // owned slash offsets
-  __shared__ float red[4][LKT];                // per wave: column sums of the tile
+  __shared__ float red[RW][LKT];               // per wave: column sums of the tile
   const int c = blockIdx.x;
   const int h = blockIdx.y;
   const int s = seq_of_chunk(a.st, c);
@@ -326,6 +329,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   const int64_t kv_row = (int64_t)a.hkv * D;
   const uint16_t *kbase = a.k + (int64_t)tok0 * kv_row + (int64_t)(h / G) * D;
   const float sl2 = a.scale * 1.4426950408889634f;
+  // a tile column's sum over the waves, in wave order
+  auto sum_waves = [&](int col) {
+    float sv = red[0][col];
+#pragma unroll
+    for (int q = 1; q < RW; ++q) sv += red[q][col];
+    return sv;
+  };
 
   // Â[r, j] = exp2(s_rj * sl2 - m_r) / (l_r * b') = exp2(s_rj * sl2 - m_r - log2(l_r * b')).
   // Lane (lr, lh) holds key lr of the tile for the 16 rows rv(v) = 32 w + 8 (v / 4) + 4 lh
@@ -346,18 +356,19 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   }
   bf16x8 qf[D / 16];
   load_qhat<D>(a, tok0, n, h, r, lh, qf);
-  for (int i = tid; i < a.st.ch_len; i += kThreads) acc_s[i] = 0.f;
-  for (int i = tid; i < LPAD * LPITCH; i += kThreads) {
+  for (int i = tid; i < a.st.ch_len; i += NT) acc_s[i] = 0.f;
+  for (int i = tid; i < LPAD * LPITCH; i += NT) {
     Pt[i] = 0.f;
-    Pt[(LPAD + 128) * LPITCH + i] = 0.f;
+    Pt[(LPAD + ROWS) * LPITCH + i] = 0.f;
   }
 
-  // keys [c0 - 128, c0) are recomputed for the diagonals owned by this chunk
-  const int kstart = max(c0 - 128, 0);
+  // keys [c0 - ROWS, c0) are recomputed for the diagonals owned by this chunk (a diagonal
+  // spans at most b' <= ROWS keys)
+  const int kstart = max(c0 - ROWS, 0);
   // two barriers per tile: after the weights (every wave's K reads are then done, so the
   // next K tile, already in registers, is stored over the current one) and after the
   // diagonal pass
-  KTile<D, kThreads, LKT> tile;
+  KTile<D, NT, LKT> tile;
   tile.load(kbase, kv_row, kstart, n, tid);
   tile.store(Ks, tid);
   if (kstart + LKT < c1) tile.load(kbase, kv_row, kstart + LKT, n, tid);
@@ -419,11 +430,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
       const int jj = kt + tid;
       if (jj < c1)
         a.a_v[(int64_t)h * a.total_tokens + tok0 + jj] =
-            ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
+            sum_waves(tid);
     }
     __syncthreads();
   }
-  for (int i = tid; i < c1 - c0; i += kThreads) {
+  for (int i = tid; i < c1 - c0; i += NT) {
     const int jl = c0 + i;
     a.a_s[(int64_t)h * a.total_tokens + tok0 + (n - 1 - jl)] = acc_s[i];
   }
@@ -504,8 +515,13 @@ hipError_t launch_rep_scores(const SelectArgs &a, hipStream_t stream) {
   }
   hipLaunchKernelGGL(rep_stats_combine, dim3(a.st.n_seq, a.hq, (a.block + 3) / 4), dim3(256), 0,
                      stream, a);
-  if (a.d == 128) hipLaunchKernelGGL(rep_lines<128>, grid, dim3(kThreads), 0, stream, a);
-  else hipLaunchKernelGGL(rep_lines<64>, grid, dim3(kThreads), 0, stream, a);
+  if (a.d == 128) {
+    if (rw == 4) hipLaunchKernelGGL((rep_lines<128, 4>), grid, dim3(64 * rw), 0, stream, a);
+    else hipLaunchKernelGGL((rep_lines<128, 2>), grid, dim3(64 * rw), 0, stream, a);
+  } else {
+    if (rw == 4) hipLaunchKernelGGL((rep_lines<64, 4>), grid, dim3(64 * rw), 0, stream, a);
+    else hipLaunchKernelGGL((rep_lines<64, 2>), grid, dim3(64 * rw), 0, stream, a);
+  }
   return hipGetLastError();
 }
 
